@@ -1,0 +1,166 @@
+/*
+ * sparseinfer.h -- C ABI of the MI355X (gfx950) SparseInfer decode path.
+ *
+ * SparseInfer (arXiv 2411.12692) predicts which rows of a ReLU-fied gated MLP
+ * produce a zero activation by comparing sign bits only (Section IV-A), then
+ * runs the MLP of Eq. (1) over the remaining rows (Section IV-B).  This
+ * library implements that per-token path with hand-written HIP kernels.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensors are DEVICE pointers allocated by the caller (the library never
+ *   allocates or frees), row-major, 16-byte aligned.  fp16 tensors are passed
+ *   as uint16_t bit patterns (IEEE binary16).
+ * - Shapes: d = model dimension, k = hidden (d_ff) dimension, b = tokens in
+ *   the decode batch.  Supported: 1 <= k <= 2^24, 128 <= d <= 8192 with
+ *   d % 128 == 0, 1 <= b <= 8.
+ * - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL means
+ *   the default stream).  Calls return after enqueueing.
+ * - Errors: arguments are validated on the host before anything is enqueued;
+ *   on any error nothing is launched, outputs are untouched, the status code
+ *   says which check failed and si_last_error() (thread-local) says why.
+ *   A failed launch returns SI_ERR_HIP.  Faults inside kernels surface at the
+ *   caller's next synchronisation, as for any HIP kernel.
+ * - Workspace: entry points that take `workspace` need a caller-owned device
+ *   buffer of at least si_workspace_bytes(k, d, b) bytes that is ZERO-FILLED
+ *   before its first use.  The library keeps it consistent from one call to
+ *   the next (it resets its own counters), so it must not be modified by the
+ *   caller afterwards, and one workspace must not be used by two calls that
+ *   can run at the same time (e.g. on two streams).
+ */
+#ifndef SPARSEINFER_H
+#define SPARSEINFER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SI_OK = 0,
+  SI_ERR_NULL = 1,      /* a required pointer is NULL                      */
+  SI_ERR_SHAPE = 2,     /* k, d or b outside the supported range           */
+  SI_ERR_ALIGN = 3,     /* a pointer is not 16-byte aligned                */
+  SI_ERR_ALPHA = 4,     /* alpha is NaN or negative                        */
+  SI_ERR_WORKSPACE = 5, /* workspace smaller than si_workspace_bytes()     */
+  SI_ERR_HIP = 6,       /* the HIP runtime reported an error               */
+  SI_ERR_FLAGS = 7      /* unknown bits in `flags`                         */
+} si_status;
+
+/* Flags of si_sparse_mlp / si_predict_sparse_mlp. */
+#define SI_NO_AS 1u /* ignore actual sparsity (Section IV-B 3): read the W_up
+                       and W_down^T rows of every predicted-active row even
+                       where h1 or h3 is zero.  Results are identical; only
+                       the work differs.  Used for the paper's +-AS ablation. */
+
+/* Human-readable reason of the last non-SI_OK status on this thread. */
+const char* si_last_error(void);
+
+/* Library version string. */
+const char* si_version(void);
+
+/*
+ * Size in bytes of the packed sign buffer of one W_gate (Section IV-B 1):
+ * one bit per element, rows padded to a multiple of 64.  Equals k*d/8 when
+ * k % 64 == 0.  Returns 0 for unsupported shapes.
+ */
+size_t si_signs_bytes(int k, int d);
+
+/*
+ * Pack the sign bits (MSBs) of W_gate, once at model load (Section IV-B 1).
+ *   w_gate : [k][d] fp16, read.
+ *   signs  : si_signs_bytes(k, d) bytes, written.  The layout is private to
+ *            the library (rows interleaved for coalesced per-row counting);
+ *            si_signs_to_canonical() exports it.
+ */
+si_status si_pack_signs(const uint16_t* w_gate, int k, int d, uint32_t* signs, void* stream);
+
+/*
+ * Export packed signs in the canonical layout: out[i][w] (k rows of d/32
+ * uint32) has bit j set iff W_gate[i][32*w + j] has its sign bit set.
+ */
+si_status si_signs_to_canonical(const uint32_t* signs, int k, int d, uint32_t* out, void* stream);
+
+/*
+ * W_down^T, once at model load (Section IV-B 4): the paper's W_down is
+ * [d][k]; the down-projection kernel skips whole rows of the [k][d]
+ * transpose.   w_down: [d][k] fp16, read.  w_down_t: [k][d] fp16, written.
+ * The two buffers must not overlap.
+ */
+si_status si_transpose_down(const uint16_t* w_down, int d, int k, uint16_t* w_down_t, void* stream);
+
+/*
+ * Integer form of Eq. (2).  A row is sparse iff alpha * N_pos < N_neg with
+ * N_pos = d - N_neg; this returns T = the smallest N_neg in [0, d] for which
+ * the row is sparse (d + 1 if none, e.g. alpha = +inf), so a row is kept
+ * iff N_neg < T.  alpha is taken as its exact float32 value; ties
+ * (alpha * N_pos == N_neg) are kept.  Returns -1 for NaN or negative alpha
+ * or unsupported d.  Host-only; needs no GPU.
+ */
+int32_t si_alpha_threshold(float alpha, int d);
+
+/* Bytes of workspace needed by si_predict / si_sparse_mlp /
+ * si_predict_sparse_mlp for these shapes (0 for unsupported shapes). */
+size_t si_workspace_bytes(int k, int d, int b);
+
+/*
+ * Predict the rows of W_gate whose ReLU output will be zero (Section IV-A).
+ * For every token t and row i: N_neg = popcount(sign(W_gate,i) XOR
+ * sign(x_t)) over the d elements, and the row is sparse for that token iff
+ * alpha * (d - N_neg) < N_neg (Eq. (2)).  A row is kept (predicted active)
+ * when at least one token keeps it.
+ *   signs      : from si_pack_signs(), read.
+ *   x          : [b][d] fp16, read.
+ *   alpha      : conservativeness, >= 0 (+inf keeps every row).
+ *   mask       : [k] uint8, written; 1 = kept, 0 = predicted sparse.
+ *   active_idx : [k] int32, written: the kept rows in ascending order in
+ *                entries 0 .. n-1 (later entries untouched).  May be NULL.
+ *   n_active   : [1] int32, written with n.  May be NULL.
+ *   workspace  : see the conventions above.
+ */
+si_status si_predict(const uint32_t* signs, int k, int d, const uint16_t* x, int b, float alpha,
+                     uint8_t* mask, int32_t* active_idx, int32_t* n_active,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Gated MLP of Eq. (1) over the kept rows (Section IV-B 3)-4)), fp32
+ * accumulation.  For every kept row i and token t:
+ *   g = W_gate,i . x_t ;  h1 = max(g, 0) ;  u = W_up,i . x_t (read only when
+ *   some token has h1 > 0) ;  h3 = h1 * u ;  y_t += h3 * W_down^T[i, :]
+ *   (row read only when some token has h3 != 0).
+ *   w_gate, w_up : [k][d] fp16; w_down_t : [k][d] fp16 (si_transpose_down).
+ *   x            : [b][d] fp16.
+ *   mask         : [k] uint8 (nonzero = kept); used only when active_idx is
+ *                  NULL, in which case the kept list is built from it.
+ *   active_idx, n_active : kept rows in ascending order and their count, as
+ *                  written by si_predict (device memory).  Either both or
+ *                  neither may be NULL.
+ *   y            : [b][d] float, overwritten.
+ *   flags        : 0 or SI_NO_AS.
+ *   counters     : [3] int32 or NULL: rows whose W_gate, W_up and W_down^T
+ *                  rows were read (n_gate, n_up, n_down).
+ */
+si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint16_t* w_down_t,
+                        int k, int d, const uint16_t* x, int b, const uint8_t* mask,
+                        const int32_t* active_idx, const int32_t* n_active, float* y,
+                        void* workspace, size_t workspace_bytes, uint32_t flags, int32_t* counters,
+                        void* stream);
+
+/*
+ * The whole per-token MLP path in one call: si_predict followed by
+ * si_sparse_mlp, with the same arguments and outputs (mask, active_idx,
+ * n_active and counters may each be NULL).  This is the decode hot path.
+ */
+si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, const uint16_t* w_up,
+                                const uint16_t* w_down_t, int k, int d, const uint16_t* x, int b,
+                                float alpha, uint8_t* mask, int32_t* active_idx, int32_t* n_active,
+                                float* y, void* workspace, size_t workspace_bytes, uint32_t flags,
+                                int32_t* counters, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARSEINFER_H */

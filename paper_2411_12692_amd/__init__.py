@@ -1,1 +1,186 @@
-"""MI355X-native SparseInfer decode path (placeholder until the binding lands)."""
+"""MI355X-native SparseInfer decode path (arXiv 2411.12692).
+
+Thin PyTorch-facing binding of ``libsparseinfer.so`` (see
+``include/sparseinfer.h``).  PyTorch only provides device memory and the
+current stream; every step of the path runs in the library's HIP kernels.
+The functions take contiguous CUDA tensors: fp16 weights/inputs (``float16``
+or ``int16`` bit patterns), and return new tensors.
+"""
+
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import _lib
+from ._lib import SI_NO_AS, SparseInferError
+
+__all__ = [
+    "SI_NO_AS", "SparseInferError", "signs_bytes", "alpha_threshold", "workspace_bytes",
+    "new_workspace", "pack_signs", "signs_to_canonical", "transpose_down", "predict",
+    "sparse_mlp", "predict_sparse_mlp", "MLPLayer",
+]
+
+
+def _vp(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtypes, ndim=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a CUDA tensor (got {t.device})")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ndim is not None and t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got {tuple(t.shape)}")
+    return t
+
+
+_F16 = (torch.float16, torch.int16)
+
+
+def signs_bytes(k: int, d: int) -> int:
+    return int(_lib.load().si_signs_bytes(k, d))
+
+
+def alpha_threshold(alpha: float, d: int) -> int:
+    """Integer form of Eq. (2): rows are kept iff N_neg < T (host only)."""
+    return int(_lib.load().si_alpha_threshold(alpha, d))
+
+
+def workspace_bytes(k: int, d: int, b: int = 1) -> int:
+    return int(_lib.load().si_workspace_bytes(k, d, b))
+
+
+def new_workspace(k: int, d: int, b: int = 1, device=None) -> torch.Tensor:
+    """Zero-filled workspace for calls with up to ``b`` tokens."""
+    n = workspace_bytes(k, d, b)
+    if n == 0:
+        raise ValueError(f"unsupported shape k={k} d={d} b={b}")
+    return torch.zeros(n, dtype=torch.uint8, device=device or "cuda")
+
+
+def pack_signs(w_gate: torch.Tensor) -> torch.Tensor:
+    """Packed sign bits of ``W_gate [k][d]`` (private layout, int32 words)."""
+    _dev(w_gate, "w_gate", _F16, 2)
+    k, d = w_gate.shape
+    nbytes = signs_bytes(k, d)
+    if nbytes == 0:
+        raise ValueError(f"unsupported shape k={k} d={d}")
+    out = torch.empty(nbytes // 4, dtype=torch.int32, device=w_gate.device)
+    _lib.call("si_pack_signs", _vp(w_gate), k, d, _vp(out), _stream())
+    return out
+
+
+def signs_to_canonical(signs: torch.Tensor, k: int, d: int) -> torch.Tensor:
+    """``[k][d/32]`` int32 words, bit j of word w = sign of element 32w+j."""
+    _dev(signs, "signs", (torch.int32,))
+    out = torch.empty(k, d // 32, dtype=torch.int32, device=signs.device)
+    _lib.call("si_signs_to_canonical", _vp(signs), k, d, _vp(out), _stream())
+    return out
+
+
+def transpose_down(w_down: torch.Tensor) -> torch.Tensor:
+    """``W_down [d][k]`` -> ``W_down^T [k][d]`` (fp16)."""
+    _dev(w_down, "w_down", _F16, 2)
+    d, k = w_down.shape
+    out = torch.empty(k, d, dtype=w_down.dtype, device=w_down.device)
+    _lib.call("si_transpose_down", _vp(w_down), d, k, _vp(out), _stream())
+    return out
+
+
+def _x2(x: torch.Tensor, d: int):
+    _dev(x, "x", _F16)
+    if x.dim() == 1:
+        x = x.view(1, -1)
+    if x.dim() != 2 or x.shape[1] != d:
+        raise ValueError(f"x must be [b][{d}], got {tuple(x.shape)}")
+    return x
+
+
+def predict(signs: torch.Tensor, x: torch.Tensor, alpha: float, k: int, workspace: torch.Tensor):
+    """Eq. (2) for every row: returns ``(mask [k] uint8, active_idx [k] int32,
+    n_active [1] int32)``; entries ``n..k-1`` of ``active_idx`` are undefined."""
+    _dev(signs, "signs", (torch.int32,))
+    d = x.shape[-1]
+    x = _x2(x, d)
+    b = x.shape[0]
+    mask = torch.empty(k, dtype=torch.uint8, device=x.device)
+    idx = torch.empty(k, dtype=torch.int32, device=x.device)
+    n = torch.empty(1, dtype=torch.int32, device=x.device)
+    _lib.call("si_predict", _vp(signs), k, d, _vp(x), b, float(alpha), _vp(mask), _vp(idx), _vp(n),
+              _vp(workspace), workspace.numel(), _stream())
+    return mask, idx, n
+
+
+def sparse_mlp(w_gate, w_up, w_down_t, x, workspace, mask=None, active_idx=None, n_active=None,
+               flags: int = 0, counters: bool = False):
+    """Eq. (1) over the kept rows; returns ``y [b][d]`` float32 (and the
+    ``[3]`` work counters when ``counters``)."""
+    for t, nm in ((w_gate, "w_gate"), (w_up, "w_up"), (w_down_t, "w_down_t")):
+        _dev(t, nm, _F16, 2)
+    k, d = w_gate.shape
+    x = _x2(x, d)
+    b = x.shape[0]
+    y = torch.empty(b, d, dtype=torch.float32, device=x.device)
+    cnt = torch.zeros(3, dtype=torch.int32, device=x.device) if counters else None
+    _lib.call("si_sparse_mlp", _vp(w_gate), _vp(w_up), _vp(w_down_t), k, d, _vp(x), b, _vp(mask),
+              _vp(active_idx), _vp(n_active), _vp(y), _vp(workspace), workspace.numel(), flags, _vp(cnt),
+              _stream())
+    return (y, cnt) if counters else y
+
+
+def predict_sparse_mlp(signs, w_gate, w_up, w_down_t, x, alpha, workspace, flags: int = 0,
+                       outputs: bool = False):
+    """The whole per-token path.  Returns ``y``; with ``outputs`` also
+    ``(mask, active_idx, n_active, counters)``."""
+    k, d = w_gate.shape
+    x = _x2(x, d)
+    b = x.shape[0]
+    y = torch.empty(b, d, dtype=torch.float32, device=x.device)
+    if outputs:
+        mask = torch.empty(k, dtype=torch.uint8, device=x.device)
+        idx = torch.empty(k, dtype=torch.int32, device=x.device)
+        n = torch.empty(1, dtype=torch.int32, device=x.device)
+        cnt = torch.zeros(3, dtype=torch.int32, device=x.device)
+    else:
+        mask = idx = n = cnt = None
+    _lib.call("si_predict_sparse_mlp", _vp(signs), _vp(w_gate), _vp(w_up), _vp(w_down_t), k, d, _vp(x), b,
+              float(alpha), _vp(mask), _vp(idx), _vp(n), _vp(y), _vp(workspace), workspace.numel(), flags,
+              _vp(cnt), _stream())
+    return (y, (mask, idx, n, cnt)) if outputs else y
+
+
+class MLPLayer:
+    """One layer's device-resident state: weights, packed signs and
+    ``W_down^T`` (both made once at load), plus a workspace."""
+
+    def __init__(self, w_gate: torch.Tensor, w_up: torch.Tensor, w_down: torch.Tensor, max_batch: int = 1,
+                 keep_w_down: bool = False):
+        self.k, self.d = w_gate.shape
+        self.w_gate = w_gate
+        self.w_up = w_up
+        self.signs = pack_signs(w_gate)
+        self.w_down_t = transpose_down(w_down)
+        self.w_down = w_down if keep_w_down else None
+        self.workspace = new_workspace(self.k, self.d, max_batch, w_gate.device)
+
+    def __call__(self, x, alpha: float, flags: int = 0, outputs: bool = False):
+        return predict_sparse_mlp(self.signs, self.w_gate, self.w_up, self.w_down_t, x, alpha, self.workspace,
+                                  flags=flags, outputs=outputs)
+
+    def predict(self, x, alpha: float):
+        return predict(self.signs, x, alpha, self.k, self.workspace)
+
+    def sparse_mlp(self, x, mask=None, active_idx=None, n_active=None, flags: int = 0, counters: bool = False):
+        return sparse_mlp(self.w_gate, self.w_up, self.w_down_t, x, self.workspace, mask, active_idx, n_active,
+                          flags, counters)

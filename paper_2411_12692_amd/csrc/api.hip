@@ -1,0 +1,228 @@
+// C ABI of libsparseinfer: argument validation, Eq. (2) threshold, launches.
+#include <cmath>
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+
+#include "../../include/sparseinfer.h"
+#include "si_device.h"
+#include "si_launch.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+si_status fail(si_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+si_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return SI_OK;
+  return fail(SI_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+#define REQUIRE_PTR(p) \
+  if (!(p)) return fail(SI_ERR_NULL, "%s is NULL", #p)
+#define REQUIRE_ALIGNED(p) \
+  if ((p) && !aligned16(p)) return fail(SI_ERR_ALIGN, "%s is not 16-byte aligned", #p)
+
+si_status check_kd(int k, int d) {
+  if (k < 1 || k > (1 << 24)) return fail(SI_ERR_SHAPE, "k=%d outside [1, 2^24]", k);
+  if (d < 128 || d > si::kMaxD || d % 128 != 0)
+    return fail(SI_ERR_SHAPE, "d=%d must be a multiple of 128 in [128, %d]", d, si::kMaxD);
+  return SI_OK;
+}
+
+si_status check_b(int b) {
+  if (b < 1 || b > si::kMaxB) return fail(SI_ERR_SHAPE, "b=%d outside [1, %d]", b, si::kMaxB);
+  return SI_OK;
+}
+
+si_status check_ws(const void* ws, size_t bytes, int k, int b) {
+  REQUIRE_PTR(ws);
+  REQUIRE_ALIGNED(ws);
+  const size_t need = si::ws_layout(k, b).total;
+  if (bytes < need) return fail(SI_ERR_WORKSPACE, "workspace of %zu bytes, %zu needed", bytes, need);
+  return SI_OK;
+}
+
+// Smallest N_neg in [0, d] for which alpha * (d - N_neg) < N_neg (Eq. (2)).
+// Both sides are exact in double: alpha has 24 significant bits and d < 2^25.
+int32_t threshold(float alpha, int d) {
+  const double a = alpha;
+  int lo = 0, hi = d;  // the predicate holds at N_neg = d (0 < d) and is monotone
+  while (lo < hi) {
+    const int mid = lo + (hi - lo) / 2;
+    if (a * (double)(d - mid) < (double)mid)
+      hi = mid;
+    else
+      lo = mid + 1;
+  }
+  return lo;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* si_last_error(void) { return g_err; }
+
+const char* si_version(void) { return "sparseinfer-gfx950 0.1"; }
+
+size_t si_signs_bytes(int k, int d) {
+  if (check_kd(k, d) != SI_OK) return 0;
+  const size_t kpad = (size_t)(k + si::kRowGroup - 1) / si::kRowGroup * si::kRowGroup;
+  return kpad * (size_t)d / 8;
+}
+
+size_t si_workspace_bytes(int k, int d, int b) {
+  if (check_kd(k, d) != SI_OK || check_b(b) != SI_OK) return 0;
+  return si::ws_layout(k, b).total;
+}
+
+int32_t si_alpha_threshold(float alpha, int d) {
+  if (std::isnan(alpha) || alpha < 0.0f) return -1;
+  if (d < 1 || d > (1 << 24)) return -1;
+  if (std::isinf(alpha)) return d + 1;
+  return threshold(alpha, d);
+}
+
+si_status si_pack_signs(const uint16_t* w_gate, int k, int d, uint32_t* signs, void* stream) {
+  REQUIRE_PTR(w_gate);
+  REQUIRE_PTR(signs);
+  REQUIRE_ALIGNED(w_gate);
+  REQUIRE_ALIGNED(signs);
+  if (si_status s = check_kd(k, d)) return s;
+  return hip_status(si::launch_pack_signs(w_gate, k, d, signs, (hipStream_t)stream), "pack_signs launch");
+}
+
+si_status si_signs_to_canonical(const uint32_t* signs, int k, int d, uint32_t* out, void* stream) {
+  REQUIRE_PTR(signs);
+  REQUIRE_PTR(out);
+  REQUIRE_ALIGNED(signs);
+  REQUIRE_ALIGNED(out);
+  if (si_status s = check_kd(k, d)) return s;
+  return hip_status(si::launch_signs_to_canonical(signs, k, d, out, (hipStream_t)stream),
+                    "signs_to_canonical launch");
+}
+
+si_status si_transpose_down(const uint16_t* w_down, int d, int k, uint16_t* w_down_t, void* stream) {
+  REQUIRE_PTR(w_down);
+  REQUIRE_PTR(w_down_t);
+  REQUIRE_ALIGNED(w_down);
+  REQUIRE_ALIGNED(w_down_t);
+  if (si_status s = check_kd(k, d)) return s;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(w_down), c = reinterpret_cast<uintptr_t>(w_down_t);
+  const uintptr_t n = (uintptr_t)k * (uintptr_t)d * 2u;
+  if (a < c + n && c < a + n) return fail(SI_ERR_SHAPE, "w_down and w_down_t overlap");
+  return hip_status(si::launch_transpose(w_down, d, k, w_down_t, (hipStream_t)stream), "transpose launch");
+}
+
+si_status si_predict(const uint32_t* signs, int k, int d, const uint16_t* x, int b, float alpha, uint8_t* mask,
+                     int32_t* active_idx, int32_t* n_active, void* workspace, size_t workspace_bytes,
+                     void* stream) {
+  REQUIRE_PTR(signs);
+  REQUIRE_PTR(x);
+  REQUIRE_PTR(mask);
+  REQUIRE_ALIGNED(signs);
+  REQUIRE_ALIGNED(x);
+  REQUIRE_ALIGNED(mask);
+  REQUIRE_ALIGNED(active_idx);
+  REQUIRE_ALIGNED(n_active);
+  if (si_status s = check_kd(k, d)) return s;
+  if (si_status s = check_b(b)) return s;
+  if (std::isnan(alpha) || alpha < 0.0f) return fail(SI_ERR_ALPHA, "alpha=%g must be >= 0 (or +inf)", (double)alpha);
+  if (si_status s = check_ws(workspace, workspace_bytes, k, b)) return s;
+  const int T = si_alpha_threshold(alpha, d);
+  return hip_status(si::launch_predict(signs, k, d, x, b, T, mask, active_idx, n_active, workspace,
+                                       (hipStream_t)stream),
+                    "predict launch");
+}
+
+si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint16_t* w_down_t, int k, int d,
+                        const uint16_t* x, int b, const uint8_t* mask, const int32_t* active_idx,
+                        const int32_t* n_active, float* y, void* workspace, size_t workspace_bytes,
+                        uint32_t flags, int32_t* counters, void* stream) {
+  REQUIRE_PTR(w_gate);
+  REQUIRE_PTR(w_up);
+  REQUIRE_PTR(w_down_t);
+  REQUIRE_PTR(x);
+  REQUIRE_PTR(y);
+  REQUIRE_ALIGNED(w_gate);
+  REQUIRE_ALIGNED(w_up);
+  REQUIRE_ALIGNED(w_down_t);
+  REQUIRE_ALIGNED(x);
+  REQUIRE_ALIGNED(y);
+  REQUIRE_ALIGNED(mask);
+  REQUIRE_ALIGNED(active_idx);
+  REQUIRE_ALIGNED(n_active);
+  REQUIRE_ALIGNED(counters);
+  if ((active_idx == nullptr) != (n_active == nullptr))
+    return fail(SI_ERR_NULL, "active_idx and n_active must both be given or both be NULL");
+  if (!active_idx && !mask) return fail(SI_ERR_NULL, "mask is NULL and no active_idx was given");
+  if (flags & ~SI_NO_AS) return fail(SI_ERR_FLAGS, "unknown flags 0x%x", flags);
+  if (si_status s = check_kd(k, d)) return s;
+  if (si_status s = check_b(b)) return s;
+  if (si_status s = check_ws(workspace, workspace_bytes, k, b)) return s;
+  hipStream_t st = (hipStream_t)stream;
+  const si::WsLayout L = si::ws_layout(k, b);
+  char* base = static_cast<char*>(workspace);
+  if (!active_idx) {
+    int32_t* idx = reinterpret_cast<int32_t*>(base + L.idx);
+    int32_t* n = reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;
+    if (si_status s = hip_status(si::launch_compact(mask, k, idx, n, st), "compact launch")) return s;
+    active_idx = idx;
+    n_active = n;
+  }
+  return hip_status(si::launch_sparse_mlp(w_gate, w_up, w_down_t, k, d, x, b, active_idx, n_active, y, workspace,
+                                          flags, counters, st),
+                    "sparse_mlp launch");
+}
+
+si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, const uint16_t* w_up,
+                                const uint16_t* w_down_t, int k, int d, const uint16_t* x, int b, float alpha,
+                                uint8_t* mask, int32_t* active_idx, int32_t* n_active, float* y, void* workspace,
+                                size_t workspace_bytes, uint32_t flags, int32_t* counters, void* stream) {
+  REQUIRE_PTR(signs);
+  REQUIRE_PTR(w_gate);
+  REQUIRE_PTR(w_up);
+  REQUIRE_PTR(w_down_t);
+  REQUIRE_PTR(x);
+  REQUIRE_PTR(y);
+  REQUIRE_ALIGNED(signs);
+  REQUIRE_ALIGNED(w_gate);
+  REQUIRE_ALIGNED(w_up);
+  REQUIRE_ALIGNED(w_down_t);
+  REQUIRE_ALIGNED(x);
+  REQUIRE_ALIGNED(y);
+  REQUIRE_ALIGNED(mask);
+  REQUIRE_ALIGNED(active_idx);
+  REQUIRE_ALIGNED(n_active);
+  REQUIRE_ALIGNED(counters);
+  if (flags & ~SI_NO_AS) return fail(SI_ERR_FLAGS, "unknown flags 0x%x", flags);
+  if (si_status s = check_kd(k, d)) return s;
+  if (si_status s = check_b(b)) return s;
+  if (std::isnan(alpha) || alpha < 0.0f) return fail(SI_ERR_ALPHA, "alpha=%g must be >= 0 (or +inf)", (double)alpha);
+  if (si_status s = check_ws(workspace, workspace_bytes, k, b)) return s;
+  const si::WsLayout L = si::ws_layout(k, b);
+  char* base = static_cast<char*>(workspace);
+  if (!mask) mask = reinterpret_cast<uint8_t*>(base + L.mask);
+  if (!active_idx) active_idx = reinterpret_cast<int32_t*>(base + L.idx);
+  if (!n_active) n_active = reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;
+  hipStream_t st = (hipStream_t)stream;
+  const int T = si_alpha_threshold(alpha, d);
+  if (si_status s = hip_status(si::launch_predict(signs, k, d, x, b, T, mask, active_idx, n_active, workspace, st),
+                               "predict launch"))
+    return s;
+  return hip_status(si::launch_sparse_mlp(w_gate, w_up, w_down_t, k, d, x, b, active_idx, n_active, y, workspace,
+                                          flags, counters, st),
+                    "sparse_mlp launch");
+}
+
+}  // extern "C"

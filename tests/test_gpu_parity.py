@@ -1,0 +1,269 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Bars: packed signs, masks, kept lists and counts bit-exact; y within 1e-2
+relative L2 (fp16 weights, fp32 accumulation; the observed error is ~1e-6,
+which the tighter secondary bound below keeps honest); work counters exact
+for n_gate and within a few rows for n_up / n_down (rows whose gate value is
+within fp32 rounding of zero may fall either way).
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2411_12692_amd as si
+from paper_2411_12692_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+ALPHAS = [0.0, 0.7, 1.0, 1.03, 1.45, 1.5, math.inf]
+DEV = "cuda"
+
+
+def u16(t: torch.Tensor) -> np.ndarray:
+    return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+
+
+def rand_bits(rng, shape, special=True):
+    vals = rng.standard_normal(shape).astype(np.float16).view(np.uint16)
+    if special:
+        pool = np.array([0x0000, 0x8000, 0x0001, 0x8001, 0x03FF, 0x7BFF, 0xFBFF], dtype=np.uint16)
+        pick = rng.random(shape) < 0.1
+        vals = np.where(pick, pool[rng.integers(0, pool.size, size=shape)], vals)
+    return vals.astype(np.uint16)
+
+
+def to_dev(a: np.ndarray) -> torch.Tensor:
+    return torch.from_numpy(a.view(np.int16).copy()).to(DEV)
+
+
+class Case:
+    """Host arrays (fp16 bits) of one layer plus its device state."""
+
+    def __init__(self, wg, wu, wd, x, max_batch=1):
+        self.wg, self.wu, self.wd, self.x = wg, wu, wd, x
+        self.k, self.d = wg.shape
+        self.layer = si.MLPLayer(to_dev(wg), to_dev(wu), to_dev(wd), max_batch=max_batch)
+        self.packed = oracle.pack_signs(wg)
+
+    @classmethod
+    def planted(cls, d, k, s, config, layer=0, b=1):
+        L = synth.planted_layer(d, k, s, config=config, layer=layer)
+        x = synth.batch_tokens(L, b, config=config)
+        return cls(u16(L.w_gate), u16(L.w_up), u16(L.w_down), u16(x), max_batch=b)
+
+
+def rel_l2(a, b):
+    nb = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / nb) if nb > 0 else float(np.linalg.norm(a))
+
+
+def check_predict(c: Case, x, alpha):
+    xd = to_dev(x)
+    mask, idx, n = c.layer.predict(xd, alpha)
+    sentinel = -7
+    idx.fill_(sentinel)
+    mask, idx2, n = si.predict(c.layer.signs, xd, alpha, c.k, c.layer.workspace)
+    # run again into a pre-filled list to check nothing past n is written
+    idx3 = torch.full((c.k,), sentinel, dtype=torch.int32, device=DEV)
+    nn3 = torch.zeros(1, dtype=torch.int32, device=DEV)
+    si._lib.call("si_predict", si._vp(c.layer.signs), c.k, c.d, si._vp(xd), x.shape[0], float(alpha),
+                 si._vp(mask), si._vp(idx3), si._vp(nn3), si._vp(c.layer.workspace), c.layer.workspace.numel(),
+                 si._stream())
+    torch.cuda.synchronize()
+    m_ref, act_ref, _ = oracle.predict_rows(c.packed, x, alpha)
+    m = mask.cpu().numpy()
+    assert np.array_equal(m, m_ref), f"alpha={alpha}: {int((m != m_ref).sum())} rows differ"
+    nref = int(m_ref.sum())
+    assert int(n.item()) == nref and int(nn3.item()) == nref
+    ref_idx = oracle.active_rows(m_ref)
+    assert np.array_equal(idx2.cpu().numpy()[:nref], ref_idx)
+    i3 = idx3.cpu().numpy()
+    assert np.array_equal(i3[:nref], ref_idx)
+    assert np.all(i3[nref:] == sentinel)
+    return m_ref
+
+
+def check_mlp(c: Case, x, mask_ref, y, counters=None, flags=0):
+    out = oracle.sparse_mlp(c.wg, c.wu, c.wd, x, mask_ref)
+    yr = out["y"]
+    yg = y.cpu().numpy().astype(np.float64)
+    err = rel_l2(yg, yr)
+    assert err <= 1e-2, err
+    scale = max(np.abs(yr).max(), 1e-30)
+    assert np.abs(yg - yr).max() <= 1e-4 * scale + 1e-30, np.abs(yg - yr).max() / scale
+    if counters is not None:
+        cnt = counters.cpu().numpy().tolist()
+        assert cnt[0] == out["n_gate"]
+        if flags & si.SI_NO_AS:
+            assert cnt[1] == cnt[2] == out["n_gate"]
+        else:
+            assert abs(cnt[1] - out["n_up"]) <= 3, (cnt, out["n_up"])
+            assert abs(cnt[2] - out["n_down"]) <= 3, (cnt, out["n_down"])
+    return out
+
+
+# ---------------------------------------------------------------------------
+# load-time steps
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("k,d", [(1, 128), (63, 128), (65, 256), (1376, 512), (200, 640), (300, 5120),
+                                 (70, 8192), (11008, 4096)])
+def test_pack_signs_bit_exact(k, d):
+    rng = np.random.default_rng(k + d)
+    w = rand_bits(rng, (k, d))
+    signs = si.pack_signs(to_dev(w))
+    can = si.signs_to_canonical(signs, k, d).cpu().numpy().view(np.uint32)
+    assert np.array_equal(can, oracle.pack_signs(w))
+
+
+@pytest.mark.parametrize("d,k", [(128, 1), (256, 65), (512, 1376), (640, 200), (4096, 300)])
+def test_transpose_exact(d, k):
+    rng = np.random.default_rng(d * 7 + k)
+    w = rand_bits(rng, (d, k))
+    out = si.transpose_down(to_dev(w))
+    assert np.array_equal(u16(out), w.T)
+
+
+# ---------------------------------------------------------------------------
+# predictor
+# ---------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def tiny():
+    return Case.planted(512, 1376, 0.9, config=1)
+
+
+@pytest.mark.parametrize("alpha", ALPHAS)
+def test_predict_tiny_all_alphas(tiny, alpha):
+    check_predict(tiny, tiny.x, alpha)
+
+
+def test_predict_random_with_special_values():
+    rng = np.random.default_rng(5)
+    wg = rand_bits(rng, (1000, 640))
+    c = Case(wg, rand_bits(rng, (1000, 640)), rand_bits(rng, (640, 1000)), rand_bits(rng, (3, 640)), max_batch=3)
+    for alpha in [0.0, 0.9, 1.0, 1.1, math.inf]:
+        check_predict(c, c.x, alpha)
+        check_predict(c, c.x[:1], alpha)
+
+
+def test_predict_repeated_calls_share_workspace(tiny):
+    for alpha in [1.0, 0.7, 1.5, 1.0, math.inf, 1.03]:
+        check_predict(tiny, tiny.x, alpha)
+
+
+@pytest.mark.parametrize("k,d", [(1, 128), (63, 128), (64, 128), (65, 384), (129, 8192), (4097, 1024)])
+def test_predict_edge_shapes(k, d):
+    rng = np.random.default_rng(k * 31 + d)
+    c = Case(rand_bits(rng, (k, d)), rand_bits(rng, (k, d)), rand_bits(rng, (d, k)), rand_bits(rng, (2, d)),
+             max_batch=2)
+    for alpha in [0.0, 1.0, 1.2]:
+        check_predict(c, c.x, alpha)
+
+
+# ---------------------------------------------------------------------------
+# sparse MLP
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("alpha", ALPHAS)
+def test_sparse_mlp_tiny_all_alphas(tiny, alpha):
+    x = to_dev(tiny.x)
+    y, (mask, idx, n, cnt) = tiny.layer(x, alpha, outputs=True)
+    torch.cuda.synchronize()
+    m_ref, _, _ = oracle.predict_rows(tiny.packed, tiny.x, alpha)
+    assert np.array_equal(mask.cpu().numpy(), m_ref)
+    check_mlp(tiny, tiny.x, m_ref, y, cnt)
+
+
+def test_separate_calls_match_fused(tiny):
+    x = to_dev(tiny.x)
+    mask, idx, n = tiny.layer.predict(x, 1.0)
+    y1, c1 = tiny.layer.sparse_mlp(x, mask, idx, n, counters=True)
+    y2 = tiny.layer.sparse_mlp(x, mask=mask)  # list built from the mask
+    y3 = tiny.layer(x, 1.0)
+    torch.cuda.synchronize()
+    m_ref = oracle.predict_rows(tiny.packed, tiny.x, 1.0)[0]
+    for y in (y1, y2, y3):
+        check_mlp(tiny, tiny.x, m_ref, y)
+    assert torch.allclose(y1, y3, rtol=1e-5, atol=1e-6)
+
+
+def test_empty_and_full_masks(tiny):
+    x = to_dev(tiny.x)
+    zero = torch.zeros(tiny.k, dtype=torch.uint8, device=DEV)
+    y, cnt = tiny.layer.sparse_mlp(x, mask=zero, counters=True)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(y).item() == 0
+    assert cnt.tolist() == [0, 0, 0]
+    ones = torch.ones(tiny.k, dtype=torch.uint8, device=DEV)
+    y, cnt = tiny.layer.sparse_mlp(x, mask=ones, counters=True)
+    torch.cuda.synchronize()
+    check_mlp(tiny, tiny.x, np.ones(tiny.k, np.uint8), y, cnt)
+
+
+def test_no_actual_sparsity_flag(tiny):
+    x = to_dev(tiny.x)
+    for alpha in [1.0, 1.5]:
+        y, (mask, _, _, cnt) = tiny.layer(x, alpha, flags=si.SI_NO_AS, outputs=True)
+        torch.cuda.synchronize()
+        m_ref = oracle.predict_rows(tiny.packed, tiny.x, alpha)[0]
+        check_mlp(tiny, tiny.x, m_ref, y, cnt, flags=si.SI_NO_AS)
+
+
+@pytest.mark.parametrize("b", [2, 3, 8])
+def test_batch_union(b):
+    c = Case.planted(512, 1376, 0.9, config=1, b=b)
+    x = to_dev(c.x)
+    for alpha in [1.0, 1.45]:
+        y, (mask, idx, n, cnt) = c.layer(x, alpha, outputs=True)
+        torch.cuda.synchronize()
+        m_ref = check_predict(c, c.x, alpha)
+        assert np.array_equal(mask.cpu().numpy(), m_ref)
+        check_mlp(c, c.x, m_ref, y, cnt)
+
+
+@pytest.mark.parametrize("k,d", [(1, 128), (63, 128), (65, 384), (129, 8192), (1000, 640)])
+def test_sparse_mlp_edge_shapes(k, d):
+    rng = np.random.default_rng(k * 17 + d)
+    c = Case(rand_bits(rng, (k, d), False), rand_bits(rng, (k, d), False), rand_bits(rng, (d, k), False),
+             rand_bits(rng, (1, d), False))
+    for alpha in [1.0, math.inf]:
+        y, (mask, _, _, cnt) = c.layer(to_dev(c.x), alpha, outputs=True)
+        torch.cuda.synchronize()
+        m_ref = oracle.predict_rows(c.packed, c.x, alpha)[0]
+        assert np.array_equal(mask.cpu().numpy(), m_ref)
+        if m_ref.any():
+            check_mlp(c, c.x, m_ref, y, cnt)
+
+
+# ---------------------------------------------------------------------------
+# full-size layers (7B and 13B shapes)
+# ---------------------------------------------------------------------------
+
+@pytest.fixture(scope="module")
+def l7b():
+    return Case.planted(4096, 11008, 0.9, config=2)
+
+
+@pytest.mark.parametrize("alpha", [0.7, 1.0, 1.03, 1.45, 1.5])
+def test_7b_layer(l7b, alpha):
+    x = to_dev(l7b.x)
+    y, (mask, idx, n, cnt) = l7b.layer(x, alpha, outputs=True)
+    torch.cuda.synchronize()
+    m_ref = check_predict(l7b, l7b.x, alpha)
+    assert np.array_equal(mask.cpu().numpy(), m_ref)
+    check_mlp(l7b, l7b.x, m_ref, y, cnt)
+
+
+def test_13b_layer():
+    c = Case.planted(5120, 13824, 0.88, config=4)
+    x = to_dev(c.x)
+    y, (mask, idx, n, cnt) = c.layer(x, 1.0, outputs=True)
+    torch.cuda.synchronize()
+    m_ref = check_predict(c, c.x, 1.0)
+    assert np.array_equal(mask.cpu().numpy(), m_ref)
+    check_mlp(c, c.x, m_ref, y, cnt)
