@@ -1,0 +1,224 @@
+"""Benchmark of the SparseInfer decode MLP path on one MI355X.
+
+One step = one pass of the whole per-token path over one layer: x-sign
+packing, sign-bit prediction (Eq. (2)), compaction, sparse gate/up with
+actual sparsity and sparse down-projection, for the 7B-shaped layer
+(d = 4096, k = 11008) with planted sparsity s = 0.9, alpha = 1.0, batch 1.
+Steps cycle through a pool of independently seeded layers whose weights
+(>= 4.4 GB) exceed the 256 MB Infinity Cache, so every step reads its bytes
+from HBM.  The timed loop is replayed from a HIP graph (the per-call host
+cost of Python would otherwise dominate a ~10 us step).
+
+Prints one JSON line.  ``value`` is the effective HBM bandwidth on the
+algorithmic bytes of a step (packed signs + x + the kept rows of W_gate,
+W_up and W_down^T + y), divided by the measured time per step.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "µs per MLP layer (predict+sparse GEMV) at 7B shape, s=0.9; effective HBM GB/s"
+D, K, S = 4096, 11008, 0.9
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_bytes(k, d, b, n_gate, n_up, n_down):
+    """Bytes the method itself must move for one layer and one step."""
+    return k * d // 8 + 2 * d * b + 2 * d * (n_gate + n_up + n_down) + 4 * d * b
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=4096)
+    ap.add_argument("--warmup", type=int, default=256)
+    ap.add_argument("--layers", type=int, default=16, help="size of the rotating layer pool")
+    ap.add_argument("--alpha", type=float, default=1.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--launches", type=int, default=256, help="individually timed launches for the roofline")
+    return ap.parse_args()
+
+
+def cpu_baseline(layers_host, alpha, budget_s):
+    """Time the CPU oracle (test infrastructure, never tuned) on a bounded
+    sample of the same workload: predict + masked MLP on the first layers of
+    the pool, repeated until the budget is spent, with one BLAS thread."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+
+    total_bytes, total_s, calls = 0.0, 0.0, 0
+    with threadpool_limits(limits=1):
+        while total_s < budget_s:
+            for wg, wu, wd, x, packed in layers_host:
+                t0 = time.perf_counter()
+                mask, _, _ = oracle.predict_rows(packed, x, alpha)
+                out = oracle.sparse_mlp(wg, wu, wd, x, mask)
+                total_s += time.perf_counter() - t0
+                calls += 1
+                total_bytes += algorithmic_bytes(K, D, x.shape[0], out["n_gate"], out["n_up"], out["n_down"])
+                if total_s >= budget_s:
+                    break
+    return {
+        "value": round(total_bytes / total_s / 1e9, 3),
+        "unit": "GB/s",
+        "us_per_layer": round(total_s / calls * 1e6, 1),
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{calls} layer calls over the first {len(layers_host)} layers of the pool "
+                  f"(predict_rows + sparse_mlp, numpy float64, 1 thread, {total_s:.1f} s)",
+        "cpu": platform.processor() or platform.machine(),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the SparseInfer MLP path is built and timed on a single "
+              "MI355X (see the sharding notes in DESIGN.md); run it with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2411_12692_amd as si
+    from paper_2411_12692_amd import synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    si._lib.load()  # fails loudly if the library is not built
+
+    L = args.layers
+    layers, xs, host = [], [], []
+    for l in range(L):
+        pl = synth.planted_layer(D, K, S, config=2, layer=l, device=dev)
+        layers.append(si.MLPLayer(pl.w_gate, pl.w_up, pl.w_down))
+        xs.append(pl.x)
+        if not args.no_cpu_baseline and l < 2:
+            def u16(t):
+                return t.cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+            wg, wu, wd, xh = u16(pl.w_gate), u16(pl.w_up), u16(pl.w_down), u16(pl.x)
+            import oracle
+            host.append((wg, wu, wd, xh, oracle.pack_signs(wg)))
+        del pl
+    torch.cuda.synchronize()
+    print(f"# pool of {L} layers ready", file=sys.stderr, flush=True)
+
+    # per-layer work counters (deterministic per layer) -> algorithmic bytes
+    ys = [torch.empty(1, D, dtype=torch.float32, device=dev) for _ in range(L)]
+    counts = []
+    for l in range(L):
+        _, (_, _, _, c) = layers[l](xs[l], args.alpha, outputs=True, y=ys[l])
+        counts.append(c)
+    torch.cuda.synchronize()
+    counts = [c.tolist() for c in counts]
+    bytes_per_layer = [algorithmic_bytes(K, D, 1, *c) for c in counts]
+    mean_bytes = sum(bytes_per_layer) / L
+
+    # graph of one pass over the pool, replayed
+    stream = torch.cuda.Stream()
+    per_graph = L * max(1, 64 // L)
+    with torch.cuda.stream(stream):
+        for i in range(per_graph):  # warm the path on the capture stream
+            layers[i % L](xs[i % L], args.alpha, y=ys[i % L])
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        for i in range(per_graph):
+            layers[i % L](xs[i % L], args.alpha, y=ys[i % L])
+    torch.cuda.synchronize()
+    reps = max(1, math.ceil(args.steps / per_graph))
+    wreps = max(1, math.ceil(args.warmup / per_graph))
+    steps, warmup = reps * per_graph, wreps * per_graph
+    for _ in range(wreps):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(reps):
+            graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = e0.elapsed_time(e1)
+    us_per_layer = gpu_ms * 1e3 / steps
+    print(f"# timed {steps} steps: {us_per_layer:.3f} us/layer (wall {wall * 1e6 / steps:.3f})",
+          file=sys.stderr, flush=True)
+
+    # roofline: individually timed launches of the layer call, queued behind a
+    # spin kernel so that host enqueue time does not enter the measurement
+    M = args.launches
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(M)]
+    with torch.cuda.stream(stream):
+        torch.cuda._sleep(int(2.4e9 * 0.02 * max(1, M / 256)))
+        for i in range(M):
+            a, b = evs[i]
+            a.record(stream)
+            layers[i % L](xs[i % L], args.alpha, y=ys[i % L])
+            b.record(stream)
+    torch.cuda.synchronize()
+    durs = [a.elapsed_time(b) * 1e3 for a, b in evs]
+    mean_launch_us = sum(durs) / M
+    mean_launch_bytes = sum(bytes_per_layer[i % L] for i in range(M)) / M
+    achieved = mean_launch_bytes / mean_launch_us / 1e3
+
+    result = {
+        "metric": METRIC,
+        "value": round(mean_bytes / us_per_layer / 1e3, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(us_per_layer / 1e3, 6),
+        "us_per_layer": round(us_per_layer, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "accumulate": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"7B-shaped ReLU gated MLP layer d={D} k={K}, planted sparsity s={S}, alpha={args.alpha}, "
+                        f"batch 1, rotating pool of {L} layers, HIP-graph replay",
+            "d": D, "k": K, "batch": 1, "alpha": args.alpha, "layers_in_pool": L,
+            "kept_rows": [c[0] for c in counts[:4]],
+            "bytes_per_layer": int(mean_bytes),
+        },
+        "roofline": {
+            "kernel": "layer call (predict+gate/up kernel and down kernel)",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "launch_us": round(mean_launch_us, 3),
+        },
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(host, args.alpha, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -54,6 +54,12 @@ typedef enum {
                        and W_down^T rows of every predicted-active row even
                        where h1 or h3 is zero.  Results are identical; only
                        the work differs.  Used for the paper's +-AS ablation. */
+#define SI_NO_SPECULATION 2u /* read W_up / W_down^T rows strictly after the
+                       values that decide whether they are needed.  By default
+                       the single-kernel path requests them early for rows
+                       whose count is far inside the Eq. (2) threshold
+                       (N_neg < T - d/16), which are almost surely active;
+                       results are identical, only the work may differ. */
 
 /* Human-readable reason of the last non-SI_OK status on this thread. */
 const char* si_last_error(void);
@@ -138,9 +144,10 @@ si_status si_predict(const uint32_t* signs, int k, int d, const uint16_t* x, int
  *                  written by si_predict (device memory).  Either both or
  *                  neither may be NULL.
  *   y            : [b][d] float, overwritten.
- *   flags        : 0 or SI_NO_AS.
+ *   flags        : 0, SI_NO_AS, SI_NO_SPECULATION or both.
  *   counters     : [3] int32 or NULL: rows whose W_gate, W_up and W_down^T
- *                  rows were read (n_gate, n_up, n_down).
+ *                  rows were read (n_gate, n_up, n_down; rows requested
+ *                  speculatively count as read).
  */
 si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint16_t* w_down_t,
                         int k, int d, const uint16_t* x, int b, const uint8_t* mask,

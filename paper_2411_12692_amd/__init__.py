@@ -14,10 +14,10 @@ import ctypes
 import torch
 
 from . import _lib
-from ._lib import SI_NO_AS, SparseInferError
+from ._lib import SI_NO_AS, SI_NO_SPECULATION, SparseInferError
 
 __all__ = [
-    "SI_NO_AS", "SparseInferError", "signs_bytes", "alpha_threshold", "workspace_bytes",
+    "SI_NO_AS", "SI_NO_SPECULATION", "SparseInferError", "signs_bytes", "alpha_threshold", "workspace_bytes",
     "new_workspace", "pack_signs", "signs_to_canonical", "transpose_down", "predict",
     "sparse_mlp", "predict_sparse_mlp", "MLPLayer",
 ]
@@ -140,13 +140,18 @@ def sparse_mlp(w_gate, w_up, w_down_t, x, workspace, mask=None, active_idx=None,
 
 
 def predict_sparse_mlp(signs, w_gate, w_up, w_down_t, x, alpha, workspace, flags: int = 0,
-                       outputs: bool = False):
-    """The whole per-token path.  Returns ``y``; with ``outputs`` also
-    ``(mask, active_idx, n_active, counters)``."""
+                       outputs: bool = False, y: torch.Tensor = None):
+    """The whole per-token path.  Returns ``y`` (written into ``y`` when
+    given); with ``outputs`` also ``(mask, active_idx, n_active, counters)``."""
     k, d = w_gate.shape
     x = _x2(x, d)
     b = x.shape[0]
-    y = torch.empty(b, d, dtype=torch.float32, device=x.device)
+    if y is None:
+        y = torch.empty(b, d, dtype=torch.float32, device=x.device)
+    else:
+        _dev(y, "y", (torch.float32,))
+        if y.numel() != b * d:
+            raise ValueError(f"y must hold [{b}][{d}] floats")
     if outputs:
         mask = torch.empty(k, dtype=torch.uint8, device=x.device)
         idx = torch.empty(k, dtype=torch.int32, device=x.device)
@@ -174,9 +179,9 @@ class MLPLayer:
         self.w_down = w_down if keep_w_down else None
         self.workspace = new_workspace(self.k, self.d, max_batch, w_gate.device)
 
-    def __call__(self, x, alpha: float, flags: int = 0, outputs: bool = False):
+    def __call__(self, x, alpha: float, flags: int = 0, outputs: bool = False, y: torch.Tensor = None):
         return predict_sparse_mlp(self.signs, self.w_gate, self.w_up, self.w_down_t, x, alpha, self.workspace,
-                                  flags=flags, outputs=outputs)
+                                  flags=flags, outputs=outputs, y=y)
 
     def predict(self, x, alpha: float):
         return predict(self.signs, x, alpha, self.k, self.workspace)

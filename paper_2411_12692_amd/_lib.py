@@ -21,6 +21,7 @@ SI_ERR_WORKSPACE = 5
 SI_ERR_HIP = 6
 SI_ERR_FLAGS = 7
 SI_NO_AS = 1
+SI_NO_SPECULATION = 2
 
 _p = ctypes.c_void_p
 _i = ctypes.c_int

@@ -166,7 +166,7 @@ si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint
   if ((active_idx == nullptr) != (n_active == nullptr))
     return fail(SI_ERR_NULL, "active_idx and n_active must both be given or both be NULL");
   if (!active_idx && !mask) return fail(SI_ERR_NULL, "mask is NULL and no active_idx was given");
-  if (flags & ~SI_NO_AS) return fail(SI_ERR_FLAGS, "unknown flags 0x%x", flags);
+  if (flags & ~(SI_NO_AS | SI_NO_SPECULATION)) return fail(SI_ERR_FLAGS, "unknown flags 0x%x", flags);
   if (si_status s = check_kd(k, d)) return s;
   if (si_status s = check_b(b)) return s;
   if (si_status s = check_ws(workspace, workspace_bytes, k, b)) return s;
@@ -205,7 +205,7 @@ si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, c
   REQUIRE_ALIGNED(active_idx);
   REQUIRE_ALIGNED(n_active);
   REQUIRE_ALIGNED(counters);
-  if (flags & ~SI_NO_AS) return fail(SI_ERR_FLAGS, "unknown flags 0x%x", flags);
+  if (flags & ~(SI_NO_AS | SI_NO_SPECULATION)) return fail(SI_ERR_FLAGS, "unknown flags 0x%x", flags);
   if (si_status s = check_kd(k, d)) return s;
   if (si_status s = check_b(b)) return s;
   if (std::isnan(alpha) || alpha < 0.0f) return fail(SI_ERR_ALPHA, "alpha=%g must be >= 0 (or +inf)", (double)alpha);
@@ -217,12 +217,19 @@ si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, c
   if (!n_active) n_active = reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;
   hipStream_t st = (hipStream_t)stream;
   const int T = si_alpha_threshold(alpha, d);
-  if (si_status s = hip_status(si::launch_predict(signs, k, d, x, b, T, mask, active_idx, n_active, workspace, st),
-                               "predict launch"))
+  if (si::layer_supported(k, d, b)) {
+    // rows with N_neg < T - d/16 are treated as surely active (speculative W_up / W_down^T requests)
+    return hip_status(si::launch_layer(signs, w_gate, w_up, w_down_t, k, d, x, b, T, d / 16, mask, active_idx,
+                                       n_active, y, workspace, flags, counters, st),
+                      "layer launch");
+  }
+  if (si_status s = hip_status(si::launch_predict_gate_up(signs, w_gate, w_up, k, d, x, b, T, mask, active_idx,
+                                                          n_active, y, workspace, flags, st),
+                               "predict/gate-up launch"))
     return s;
-  return hip_status(si::launch_sparse_mlp(w_gate, w_up, w_down_t, k, d, x, b, active_idx, n_active, y, workspace,
-                                          flags, counters, st),
-                    "sparse_mlp launch");
+  return hip_status(si::launch_down(w_down_t, k, d, b, active_idx, n_active, y, workspace, si::row_groups(k), flags,
+                                    counters, st),
+                    "down-projection launch");
 }
 
 }  // extern "C"

@@ -1,23 +1,28 @@
 // Sign-bit activation-sparsity predictor (Section IV-A, Eq. (2)) with ordered
-// compaction of the kept rows.
+// compaction of the kept rows, optionally fused with the sparse gate/up GEMV
+// (Section IV-B 3)-4): steps 1-3 of Eq. (1) for the kept rows).
 //
-// One block of 4 wavefronts handles one group of 64 rows; lane r of every
-// wave owns row 64*v + r (lane-per-row: no cross-lane reduction, and a
-// wave-wide ballot gives the group's kept rows directly).  The 4 waves split
-// the row's packed words and add their counts through LDS.  The sign words of
-// x (one token or up to 8) are packed by the block itself into LDS.
+// One block of 8 wavefronts owns one group of 64 rows (blockIdx = group).
+//  1. x is staged in LDS and its sign words are packed there.
+//  2. Lane r of every wave counts N_neg of row 64*g + r over an eighth of the
+//     row's packed words (XOR + popcount, 16-byte coalesced loads from the
+//     interleaved sign layout); the 8 partial counts meet in LDS.
+//  3. Wave 0 applies Eq. (2) through the host-computed integer threshold T
+//     (kept iff N_neg < T for some token), writes the mask, and ballots the
+//     kept rows into an LDS list.
+//  4. Fused variant: waves 1..7 stream the W_gate row of each kept row, and
+//     the W_up row only where some token's ReLU output is positive (actual
+//     sparsity), writing h3 = h1 * u per row.
+//  5. Meanwhile wave 0 finds the group's offset in the ascending kept list
+//     with a decoupled look-back: it posts its count, then reads up to 64
+//     predecessors' posted words at once (one per lane) until it meets an
+//     inclusive prefix.  It then writes its kept rows at that offset.
 //
-// Eq. (2) is applied through the integer threshold T computed on the host:
-// a row is kept for a token iff N_neg < T.
-//
-// The ascending kept list needs each group's offset, i.e. an exclusive
-// prefix over the groups' counts.  It is obtained in the same pass with a
-// decoupled look-back: blocks take their group id from a ticket counter (so
-// a block only ever waits on groups owned by blocks that already run), post
-// their own count, and walk back over their predecessors' posted counts.
-// Posted words carry a call counter (epoch) so the workspace never needs to
-// be cleared between calls; the last block of a call resets the ticket and
-// advances the epoch.
+// Posted words carry a per-call counter (epoch) so the workspace is never
+// cleared between calls.  The last group advances the epoch once its
+// look-back completes: by then every group has posted, so every block has
+// read the current epoch.  No single-address atomic counters are used (they
+// serialise across the chip).
 #include "si_device.h"
 #include "si_launch.h"
 
@@ -25,89 +30,83 @@ namespace si {
 
 constexpr uint64_t kFlagAggregate = 1ull << 30;  // count of this group only
 constexpr uint64_t kFlagPrefix = 2ull << 30;     // inclusive prefix up to this group
-constexpr long kSpinLimit = 1l << 22;
+constexpr uint64_t kFlagMask = 3ull << 30;
+constexpr long kSpinLimit = 1l << 20;
+constexpr int kPredWaves = 8;
 
-// Returns the number of kept rows in groups 0 .. v-1.
-__device__ int lookback(uint64_t* status, int v, int local, uint32_t epoch, uint32_t* hdr) {
-  const uint64_t tag = (uint64_t)epoch << 32;
-  if (v == 0) {
-    st_agent64(&status[0], tag | kFlagPrefix | (uint64_t)local);
-    return 0;
-  }
-  st_agent64(&status[v], tag | kFlagAggregate | (uint64_t)local);
+// Wave-wide look-back: returns the number of kept rows in groups 0 .. v-1.
+// The caller has already posted the group's aggregate.
+__device__ int lookback_wave(const uint64_t* status, int v, uint32_t tag, int lane, uint32_t* hdr) {
   int excl = 0;
   int j = v - 1;
   long spins = 0;
   while (j >= 0) {
-    const uint64_t s = ld_agent64(&status[j]);
-    const uint64_t flag = s & (3ull << 30);
-    if ((uint32_t)(s >> 32) != epoch || flag == 0) {
-      if (++spins > kSpinLimit) {  // never expected: predecessors are running
-        atomicOr(&hdr[H_ERR], kErrLookbackSpin);
+    const int jj = j - lane;  // lane 0 = nearest predecessor
+    uint64_t s = 0;
+    bool ready = true, prefix = true;
+    if (jj >= 0) {
+      s = ld_agent64(&status[jj]);
+      ready = (uint32_t)(s >> 32) == tag && (s & kFlagMask) != 0;
+      prefix = ready && (s & kFlagMask) == kFlagPrefix;
+    }
+    const uint64_t pmask = __ballot(prefix);
+    const uint64_t rmask = __ballot(ready);
+    const int first = pmask ? __builtin_ctzll(pmask) : kWave;
+    const uint64_t need = first >= kWave - 1 ? ~0ull : ((2ull << first) - 1ull);
+    if ((rmask & need) != need) {
+      if (++spins > kSpinLimit) {  // never expected: every group posts right after counting
+        if (lane == 0) atomicOr(&hdr[H_ERR], kErrLookbackSpin);
         break;
       }
       __builtin_amdgcn_s_sleep(1);
       continue;
     }
-    excl += (int)(s & 0x3fffffffu);
-    if (flag == kFlagPrefix) break;
-    --j;
+    const int val = (jj >= 0 && lane <= first) ? (int)(s & 0x3fffffffu) : 0;
+    excl += wave_sum_int(val);
+    if (first < kWave) break;
+    j -= kWave;
   }
-  st_agent64(&status[v], tag | kFlagPrefix | (uint64_t)(excl + local));
   return excl;
 }
 
-// Count this block as finished; the last block of the call resets the ticket
-// and advances the epoch for the next call.
-__device__ inline void finish_predict(uint32_t* hdr, int groups, uint32_t epoch) {
-  const uint32_t done = atomicAdd(&hdr[H_PRED_DONE], 1u);
-  if (done == (uint32_t)groups - 1) {  // every block has taken its ticket and finished
-    st_agent(&hdr[H_PRED_TICKET], 0u);
-    st_agent(&hdr[H_PRED_DONE], 0u);
-    st_agent(&hdr[H_PRED_EPOCH], epoch + 1u);
-  }
-}
-
-template <int B>
-__global__ __launch_bounds__(256) void k_predict(const u32x4* __restrict__ signs, int k, int d,
-                                                 const uint16_t* __restrict__ x, int T,
-                                                 uint8_t* __restrict__ mask, int32_t* __restrict__ idx,
-                                                 int32_t* __restrict__ n_out, uint64_t* __restrict__ status,
-                                                 uint32_t* __restrict__ hdr) {
+template <int B, bool FUSED>
+__global__ __launch_bounds__(kPredWaves * kWave) void k_rows(
+    const u32x4* __restrict__ signs, int k, int d, const uint16_t* __restrict__ x, int T,
+    uint8_t* __restrict__ mask, int32_t* __restrict__ idx, int32_t* __restrict__ n_out,
+    uint64_t* __restrict__ status, uint32_t* __restrict__ hdr,
+    const u32x4* __restrict__ wg, const u32x4* __restrict__ wu, float* __restrict__ h3row,
+    uint8_t* __restrict__ upflag, int32_t* __restrict__ counts, float* __restrict__ y, uint32_t flags) {
+  extern __shared__ u32x4 xs[];  // [B][d/8] fp16 tokens
   __shared__ __attribute__((aligned(16))) uint32_t xw[B * (kMaxD / 32)];
-  __shared__ int cnt[4][B][kWave];
-  __shared__ uint32_t s_v, s_epoch;
+  __shared__ int cnt[kPredWaves][B][kWave];
+  __shared__ int kept[kRowGroup];
+  __shared__ int s_nkept, s_up, s_down;
+  constexpr int NT = kPredWaves * kWave;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int W = d >> 5, units = W >> 2;
-  const int groups = (k + kRowGroup - 1) / kRowGroup;
-
-  if (tid == 0) {
-    s_v = atomicAdd(&hdr[H_PRED_TICKET], 1u);
-    s_epoch = ld_agent(&hdr[H_PRED_EPOCH]);
-  }
-  // sign words of the b input tokens
-  for (int t = tid; t < B * W; t += 256) {
-    const int tok = t / W, w = t - tok * W;
-    xw[t] = sign_word(reinterpret_cast<const u32x4*>(x + (size_t)tok * d + 32 * w));
-  }
-  __syncthreads();
-  const int v = (int)s_v;
-  const uint32_t epoch = s_epoch;
-  if (v >= groups) {  // only if the workspace was not zero-filled before first use
-    if (tid == 0) {
-      atomicOr(&hdr[H_ERR], kErrTicket);
-      finish_predict(hdr, groups, epoch);
-    }
-    return;
-  }
+  const int U = d >> 3, W = d >> 5, units = W >> 2;
+  const int v = blockIdx.x;
+  const int groups = gridDim.x;
   const int row = v * kRowGroup + lane;
 
+  if (FUSED && v == 0) {  // y is accumulated with atomics by the down-projection kernel
+    for (int i = tid; i < B * d; i += NT) y[i] = 0.f;
+  }
+  // 1. tokens -> LDS, then their packed sign words
+  for (int i = tid; i < B * U; i += NT) xs[i] = reinterpret_cast<const u32x4*>(x)[i];
+  __syncthreads();
+  for (int i = tid; i < B * W; i += NT) {
+    const int t = i / W, w = i - t * W;
+    xw[i] = sign_word(&xs[t * U + 4 * w]);
+  }
+  __syncthreads();
+
+  // 2. N_neg partial counts
   int c[B];
 #pragma unroll
   for (int t = 0; t < B; ++t) c[t] = 0;
   const u32x4* sg = signs + (size_t)v * units * kRowGroup + lane;
 #pragma unroll 4
-  for (int q = wv; q < units; q += 4) {
+  for (int q = wv; q < units; q += kPredWaves) {
     const u32x4 s = load_nt(sg + (size_t)q * kRowGroup);
 #pragma unroll
     for (int t = 0; t < B; ++t) {
@@ -118,27 +117,120 @@ __global__ __launch_bounds__(256) void k_predict(const u32x4* __restrict__ signs
 #pragma unroll
   for (int t = 0; t < B; ++t) cnt[wv][t][lane] = c[t];
   __syncthreads();
-  if (wv != 0) return;
 
-  bool keep = false;
+  // 3. Eq. (2), mask, kept list in LDS, post this group's count
+  uint64_t ballot = 0;
+  uint32_t epoch = 0;
+  if (wv == 0) {
+    bool keep = false;
 #pragma unroll
-  for (int t = 0; t < B; ++t) {
-    const int n_neg = cnt[0][t][lane] + cnt[1][t][lane] + cnt[2][t][lane] + cnt[3][t][lane];
-    keep |= n_neg < T;
+    for (int t = 0; t < B; ++t) {
+      int n_neg = 0;
+#pragma unroll
+      for (int w = 0; w < kPredWaves; ++w) n_neg += cnt[w][t][lane];
+      keep |= n_neg < T;
+    }
+    keep = keep && row < k;
+    if (row < k) mask[row] = keep ? 1 : 0;
+    ballot = __ballot(keep);
+    const int local = __popcll(ballot);
+    if (keep) kept[__popcll(ballot & lanes_below(lane))] = row;
+    if (lane == 0) {
+      s_nkept = local;
+      s_up = 0;
+      s_down = 0;
+      epoch = ld_agent(&hdr[H_PRED_EPOCH]);
+      const uint64_t tag = (uint64_t)epoch_tag(epoch) << 32;
+      st_agent64(&status[v], tag | (v == 0 ? kFlagPrefix : kFlagAggregate) | (uint64_t)local);
+    }
+    epoch = __shfl(epoch, 0, kWave);
   }
-  keep = keep && row < k;
-  if (row < k) mask[row] = keep ? 1 : 0;
-  const uint64_t ballot = __ballot(keep);
-  const int local = __popcll(ballot);
-  int excl = 0;
-  if (lane == 0) excl = lookback(status, v, local, epoch, hdr);
-  excl = __shfl(excl, 0, kWave);
-  if (keep && idx) idx[excl + __popcll(ballot & lanes_below(lane))] = row;
-  if (lane == 0) {
-    if (v == groups - 1 && n_out) *n_out = excl + local;
-    finish_predict(hdr, groups, epoch);
+  __syncthreads();
+  const int nkept = s_nkept;
+
+  if (wv == 0) {
+    // 5. offset of this group in the ascending kept list
+    const int excl = v == 0 ? 0 : lookback_wave(status, v, epoch_tag(epoch), lane, hdr);
+    if (lane == 0 && v > 0)
+      st_agent64(&status[v], ((uint64_t)epoch_tag(epoch) << 32) | kFlagPrefix | (uint64_t)(excl + nkept));
+    if (lane < nkept && idx) idx[excl + lane] = kept[lane];
+    if (lane == 0 && v == groups - 1) {
+      if (n_out) *n_out = excl + nkept;
+      st_agent(&hdr[H_PRED_EPOCH], epoch + 1u);  // every group has posted: all read this epoch
+    }
+  } else if (FUSED) {
+    // 4. sparse gate/up over the kept rows of this group
+    int n_up = 0, n_down = 0;
+    const bool no_as = (flags & 1u) != 0;
+    for (int i = wv - 1; i < nkept; i += kPredWaves - 1)
+      gate_up_row<B>(wg, wu, kept[i], U, xs, lane, no_as, h3row, upflag, n_up, n_down);
+    if (lane == 0 && (n_up | n_down)) {
+      atomicAdd(&s_up, n_up);
+      atomicAdd(&s_down, n_down);
+    }
+  }
+  if (FUSED) {
+    __syncthreads();
+    if (tid == 0) {
+      counts[2 * v] = s_up;
+      counts[2 * v + 1] = s_down;
+    }
   }
 }
+
+template <int B, bool FUSED>
+static hipError_t rows_b(const uint32_t* signs, int k, int d, const uint16_t* x, int T, uint8_t* mask,
+                         int32_t* idx, int32_t* n_out, void* ws, const uint16_t* w_gate, const uint16_t* w_up,
+                         float* y, uint32_t flags, hipStream_t s) {
+  const WsLayout L = ws_layout(k, B);
+  char* base = static_cast<char*>(ws);
+  const size_t lds = (size_t)B * d * sizeof(uint16_t);
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_rows<B, FUSED>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)((size_t)kMaxB * kMaxD * sizeof(uint16_t)));
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  k_rows<B, FUSED><<<row_groups(k), kPredWaves * kWave, lds, s>>>(
+      reinterpret_cast<const u32x4*>(signs), k, d, x, T, mask, idx, n_out,
+      reinterpret_cast<uint64_t*>(base + L.status), reinterpret_cast<uint32_t*>(base),
+      reinterpret_cast<const u32x4*>(w_gate), reinterpret_cast<const u32x4*>(w_up),
+      reinterpret_cast<float*>(base + L.h3), reinterpret_cast<uint8_t*>(base + L.upflag),
+      reinterpret_cast<int32_t*>(base + L.counts), y, flags);
+  return hipGetLastError();
+}
+
+#define SI_ROWS_CASES(FUSED)                                                                              \
+  switch (b) {                                                                                            \
+    case 1: return rows_b<1, FUSED>(signs, k, d, x, T, mask, idx, n_out, ws, w_gate, w_up, y, flags, s); \
+    case 2: return rows_b<2, FUSED>(signs, k, d, x, T, mask, idx, n_out, ws, w_gate, w_up, y, flags, s); \
+    case 3: return rows_b<3, FUSED>(signs, k, d, x, T, mask, idx, n_out, ws, w_gate, w_up, y, flags, s); \
+    case 4: return rows_b<4, FUSED>(signs, k, d, x, T, mask, idx, n_out, ws, w_gate, w_up, y, flags, s); \
+    case 5: return rows_b<5, FUSED>(signs, k, d, x, T, mask, idx, n_out, ws, w_gate, w_up, y, flags, s); \
+    case 6: return rows_b<6, FUSED>(signs, k, d, x, T, mask, idx, n_out, ws, w_gate, w_up, y, flags, s); \
+    case 7: return rows_b<7, FUSED>(signs, k, d, x, T, mask, idx, n_out, ws, w_gate, w_up, y, flags, s); \
+    case 8: return rows_b<8, FUSED>(signs, k, d, x, T, mask, idx, n_out, ws, w_gate, w_up, y, flags, s); \
+    default: return hipErrorInvalidValue;                                                                 \
+  }
+
+hipError_t launch_predict(const uint32_t* signs, int k, int d, const uint16_t* x, int b, int T,
+                          uint8_t* mask, int32_t* idx, int32_t* n_out, void* ws, hipStream_t s) {
+  const uint16_t* w_gate = nullptr;
+  const uint16_t* w_up = nullptr;
+  float* y = nullptr;
+  const uint32_t flags = 0;
+  SI_ROWS_CASES(false)
+}
+
+hipError_t launch_predict_gate_up(const uint32_t* signs, const uint16_t* w_gate, const uint16_t* w_up, int k,
+                                  int d, const uint16_t* x, int b, int T, uint8_t* mask, int32_t* idx,
+                                  int32_t* n_out, float* y, void* ws, uint32_t flags, hipStream_t s) {
+  SI_ROWS_CASES(true)
+}
+
+#undef SI_ROWS_CASES
 
 // mask -> ascending list of the nonzero positions and their count.
 __global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ mask, int k,
@@ -166,33 +258,6 @@ __global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ ma
     __syncthreads();
   }
   if (tid == 0) *n_out = base;
-}
-
-template <int B>
-static void predict_b(const uint32_t* signs, int k, int d, const uint16_t* x, int T, uint8_t* mask,
-                      int32_t* idx, int32_t* n_out, void* ws, hipStream_t s) {
-  const WsLayout L = ws_layout(k, B);
-  char* base = static_cast<char*>(ws);
-  const int groups = (k + kRowGroup - 1) / kRowGroup;
-  k_predict<B><<<groups, 256, 0, s>>>(reinterpret_cast<const u32x4*>(signs), k, d, x, T, mask, idx, n_out,
-                                       reinterpret_cast<uint64_t*>(base + L.status),
-                                       reinterpret_cast<uint32_t*>(base));
-}
-
-hipError_t launch_predict(const uint32_t* signs, int k, int d, const uint16_t* x, int b, int T,
-                          uint8_t* mask, int32_t* idx, int32_t* n_out, void* ws, hipStream_t s) {
-  switch (b) {
-    case 1: predict_b<1>(signs, k, d, x, T, mask, idx, n_out, ws, s); break;
-    case 2: predict_b<2>(signs, k, d, x, T, mask, idx, n_out, ws, s); break;
-    case 3: predict_b<3>(signs, k, d, x, T, mask, idx, n_out, ws, s); break;
-    case 4: predict_b<4>(signs, k, d, x, T, mask, idx, n_out, ws, s); break;
-    case 5: predict_b<5>(signs, k, d, x, T, mask, idx, n_out, ws, s); break;
-    case 6: predict_b<6>(signs, k, d, x, T, mask, idx, n_out, ws, s); break;
-    case 7: predict_b<7>(signs, k, d, x, T, mask, idx, n_out, ws, s); break;
-    case 8: predict_b<8>(signs, k, d, x, T, mask, idx, n_out, ws, s); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
 }
 
 hipError_t launch_compact(const uint8_t* mask, int k, int32_t* idx, int32_t* n_out, hipStream_t s) {

@@ -17,40 +17,50 @@ constexpr int kTile = 512;      // columns of y handled by one down-projection b
 
 // Header words at the start of the workspace.
 enum : int {
-  H_PRED_TICKET = 0,  // next virtual row-group id of the predictor
-  H_PRED_EPOCH = 1,   // call counter tagging the predictor's look-back words
-  H_PRED_DONE = 2,    // predictor blocks finished in this call
-  H_ERR = 3,          // sticky device-side error bits
-  H_N_UP = 4,         // rows whose W_up row was read (this call)
-  H_N_DOWN = 5,       // rows whose W_down^T row was read (this call)
-  H_DOWN_DONE = 6,    // down-projection blocks finished in this call
-  H_N_INTERNAL = 7,   // kept-row count when the list lives in the workspace
+  H_PRED_EPOCH = 0,   // call counter tagging the predictor's look-back words
+  H_ERR = 1,          // sticky device-side error bits
+  H_N_INTERNAL = 2,   // kept-row count when the list lives in the workspace
   H_WORDS = 64
 };
 
 constexpr uint32_t kErrLookbackSpin = 1u;  // a look-back wait hit its spin limit
-constexpr uint32_t kErrTicket = 2u;        // predictor ticket out of range
 constexpr uint32_t kErrRow = 4u;           // kept-row index outside [0, k)
+
+constexpr int kGateUpMaxBlocks = 2048;     // grid cap of the list-driven gate/up kernel
 
 // Workspace layout (byte offsets), identical on host and device.
 struct WsLayout {
   size_t status;  // uint64 look-back word per row group
+  size_t counts;  // int32 [slots][2]: rows whose W_up / W_down^T row was read, per block
   size_t idx;     // int32 [k] kept rows (when the caller gives none)
   size_t mask;    // uint8 [k] mask (when the caller gives none)
-  size_t h3;      // float [k][b] h3 of each kept position
+  size_t upflag;  // uint8 [k] 1 where the W_up row was read
+  size_t h3;      // float [k][b] h3 per row (valid on kept rows)
+  size_t layer;   // single-kernel exchange words: [groups] + [groups][64] + [groups][64][b] + [64] uint64
   size_t total;
 };
 
 __host__ __device__ inline size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
+__host__ __device__ inline int row_groups(int k) { return (k + kRowGroup - 1) / kRowGroup; }
+
+__host__ __device__ inline int count_slots(int k) {
+  const int g = row_groups(k);
+  return g > kGateUpMaxBlocks ? g : kGateUpMaxBlocks;
+}
+
 __host__ __device__ inline WsLayout ws_layout(int k, int b) {
   WsLayout L;
-  const size_t groups = (size_t)(k + kRowGroup - 1) / kRowGroup;
+  const size_t groups = (size_t)row_groups(k);
   L.status = align256(H_WORDS * sizeof(uint32_t));
-  L.idx = L.status + align256(groups * sizeof(uint64_t));
+  L.counts = L.status + align256(groups * sizeof(uint64_t));
+  L.idx = L.counts + align256((size_t)count_slots(k) * 2 * sizeof(int32_t));
   L.mask = L.idx + align256((size_t)k * sizeof(int32_t));
-  L.h3 = L.mask + align256((size_t)k);
-  L.total = L.h3 + align256((size_t)k * b * sizeof(float));
+  L.upflag = L.mask + align256((size_t)k);
+  L.h3 = L.upflag + align256((size_t)k);
+  L.layer = L.h3 + align256((size_t)k * b * sizeof(float));
+  L.total = L.layer + align256(groups * 8) + align256(groups * kRowGroup * 8) +
+            align256(groups * kRowGroup * (size_t)b * 8) + align256(64 * 8);
   return L;
 }
 
@@ -82,11 +92,21 @@ __device__ inline float wave_sum(float v) {
   return v;
 }
 
+__device__ inline int wave_sum_int(int v) {
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, kWave);
+  return v;
+}
+
 __device__ inline u32x4 load_nt(const u32x4* p) { return __builtin_nontemporal_load(p); }
 
 __device__ inline uint64_t lanes_below(int lane) {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
+
+// Tag that marks a word as written in the call with this epoch.  The high
+// bit is always set, so a zero-filled workspace never carries a valid tag.
+__device__ inline uint32_t epoch_tag(uint32_t epoch) { return (epoch & 0x7fffffffu) | 0x80000000u; }
 
 __device__ inline uint32_t ld_agent(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -99,6 +119,71 @@ __device__ inline uint64_t ld_agent64(const uint64_t* p) {
 }
 __device__ inline void st_agent64(uint64_t* p, uint64_t v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+constexpr int kMaxUnitsPerLane = kMaxD / 8 / kWave;  // 16-byte units of a row per lane (16)
+
+// Dot products of one [d] fp16 row (U = d/8 16-byte units, streamed with
+// non-temporal loads) with B tokens staged in LDS as xs[t][U].  Every load of
+// the row is issued before the first product.  Result in every lane.
+template <int B>
+__device__ inline void row_dot(const u32x4* __restrict__ row, const u32x4* xs, int U, int lane, float (&out)[B]) {
+  u32x4 w[kMaxUnitsPerLane];
+#pragma unroll
+  for (int j = 0; j < kMaxUnitsPerLane; ++j) {
+    const int u = lane + kWave * j;
+    if (u < U) w[j] = load_nt(row + u);
+  }
+  float acc[B];
+#pragma unroll
+  for (int t = 0; t < B; ++t) acc[t] = 0.f;
+#pragma unroll
+  for (int j = 0; j < kMaxUnitsPerLane; ++j) {
+    const int u = lane + kWave * j;
+    if (u < U) {
+#pragma unroll
+      for (int t = 0; t < B; ++t) acc[t] = dot8(w[j], xs[t * U + u], acc[t]);
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < B; ++t) out[t] = wave_sum(acc[t]);
+}
+
+// Gate/up of one kept row (Eq. (1) steps 1-3 with actual sparsity): returns
+// through h[] the B values h3 = ReLU(W_gate,row . x) * (W_up,row . x); the
+// W_up row is read only if some token has a positive gate value (or always
+// with no_as).  Stores h3 per row, the up-read flag, and counts the work.
+template <int B>
+__device__ inline void gate_up_row(const u32x4* __restrict__ wg, const u32x4* __restrict__ wu, int row, int U,
+                                   const u32x4* xs, int lane, bool no_as, float* __restrict__ h3row,
+                                   uint8_t* __restrict__ upflag, int& n_up, int& n_down) {
+  float g[B];
+  row_dot<B>(wg + (size_t)row * U, xs, U, lane, g);
+  bool any = false;
+#pragma unroll
+  for (int t = 0; t < B; ++t) {
+    g[t] = fmaxf(g[t], 0.f);
+    any |= g[t] > 0.f;
+  }
+  float h[B];
+#pragma unroll
+  for (int t = 0; t < B; ++t) h[t] = 0.f;
+  const bool up = any || no_as;
+  if (up) {
+    float u[B];
+    row_dot<B>(wu + (size_t)row * U, xs, U, lane, u);
+#pragma unroll
+    for (int t = 0; t < B; ++t) h[t] = g[t] * u[t];
+  }
+  bool nz = false;
+#pragma unroll
+  for (int t = 0; t < B; ++t) nz |= h[t] != 0.f;
+  n_up += up ? 1 : 0;
+  n_down += (nz || no_as) ? 1 : 0;
+#pragma unroll
+  for (int t = 0; t < B; ++t)
+    if (lane == t) h3row[(size_t)row * B + t] = h[t];
+  if (lane == 0) upflag[row] = up ? 1 : 0;
 }
 
 }  // namespace si

@@ -120,7 +120,7 @@ def test_validation_errors(lib):
         ("si_predict", (_p(A), 128, 256, _p(A), 1, 1.0, _p(A), None, None, None, ws, None), _lib.SI_ERR_NULL),
         ("si_sparse_mlp", (_p(A), _p(A), _p(A), 128, 256, _p(A), 1, _p(A), _p(A), None, _p(A), _p(A), ws, 0,
                            None, None), _lib.SI_ERR_NULL),
-        ("si_sparse_mlp", (_p(A), _p(A), _p(A), 128, 256, _p(A), 1, _p(A), None, None, _p(A), _p(A), ws, 2,
+        ("si_sparse_mlp", (_p(A), _p(A), _p(A), 128, 256, _p(A), 1, _p(A), None, None, _p(A), _p(A), ws, 4,
                            None, None), _lib.SI_ERR_FLAGS),
         ("si_sparse_mlp", (_p(A), _p(A), _p(A), 128, 256, _p(A), 1, None, None, None, _p(A), _p(A), ws, 0,
                            None, None), _lib.SI_ERR_NULL),
