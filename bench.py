@@ -205,7 +205,7 @@ def main():
             "bytes_per_layer": int(mean_bytes),
         },
         "roofline": {
-            "kernel": "layer call (predict+gate/up kernel and down kernel)",
+            "kernel": "k_layer (predict + compaction + gate/up + down, one launch per layer)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,

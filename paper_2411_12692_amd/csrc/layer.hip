@@ -2,44 +2,53 @@
 // prediction (Section IV-A, Eq. (2)), ordered compaction, sparse gate/up with
 // actual sparsity and sparse down-projection (Section IV-B 3)-4)).
 //
-// One block of 16 wavefronts per group of 64 rows (all blocks co-resident;
-// the host only takes this path when they fit).  Roles inside a block:
+// One block of 12 wavefronts per group of 64 rows; all blocks are resident
+// at once (the host takes this path only when they fit).  Groups are cut
+// into chunks of consecutive groups; a down-projection work item is a
+// (512-column tile of y, chunk) pair, at most one per block.
 //
-//  all waves   issue the group's packed-sign loads first, stage x in LDS,
-//              pack its sign words, and add their XOR/popcount partials.
-//  wave 0      applies Eq. (2) (N_neg < T), writes the mask, publishes the
-//              group's kept list, then runs the look-back that places the
-//              group in the ascending kept list (active_idx) and, in the last
-//              group, writes the count and advances the epoch.
-//  waves 1-7   gate/up of the group's kept rows: W_gate row, and W_up row only
-//              where some token's ReLU output is positive.  Rows whose count
-//              is far inside the threshold (N_neg < T - margin) are almost
-//              surely positive, so their W_up row is requested together with
-//              the W_gate row instead of one memory round trip later.
-//  waves 8-15  down-projection of one work item = (512-column tile of y,
-//              chunk of consecutive groups).  They read the chunk's kept
-//              lists as soon as they are published and request the W_down^T
-//              row segments of the confident rows at once, overlapping the
-//              gate/up phase, then collect h3 and finish the other rows.
-//              The block's partial tile is reduced in LDS and added into y
-//              with fp32 atomics; tile c is zeroed first by block c.
+//  all waves    issue the group's packed-sign loads first, stage x in LDS,
+//               pack its sign words and add their XOR/popcount partials.
+//  wave 0       applies Eq. (2) (kept iff N_neg < T), writes the mask,
+//               publishes the group's kept and "confident" masks (rows with
+//               N_neg < T - margin, almost surely active), then places the
+//               group in the ascending kept list with a wave-wide look-back.
+//  waves 1-7    gate/up: the kept rows of the block's chunk are split evenly
+//               over the chunk's blocks (balancing groups with many kept
+//               rows); for each row the W_gate row is streamed and the W_up
+//               row too where some token's ReLU output is positive (requested
+//               together with W_gate for confident rows); h3 is published
+//               per chunk position.
+//  waves 8-11   down-projection of the block's item: they read the chunk's
+//               masks, request the W_down^T row segments of the confident
+//               rows at once (overlapping the gate/up traffic), collect h3
+//               and finish the other rows, reduce in LDS and add the tile
+//               into y with fp32 atomics once block `tile` has zeroed it.
 //
-// Blocks exchange data through epoch-tagged 64-bit words (tag = call
-// counter in the high half, payload in the low half) written and polled with
-// agent-scope relaxed atomics: a consumer polls each word until it carries
-// the current epoch, so no cache flushes or fences are needed, and the
-// workspace is never cleared between calls.  Every poll has a spin limit that
-// sets an error bit instead of hanging.
+// Blocks exchange data through epoch-tagged 64-bit words (tag = per-call
+// counter with the high bit set, in the high half; payload in the low half)
+// written with agent-scope write-through stores and polled one word per lane
+// with agent-scope loads: a word is valid once it carries the call's tag, so
+// no cache flush or fence is needed and the workspace is never cleared
+// between calls.  Every poll has a spin limit that sets an error bit instead
+// of hanging.
 #include "si_device.h"
 #include "si_launch.h"
 
 namespace si {
 
-constexpr int kLayerWaves = 16;
+#ifdef SI_TRACE
+__device__ uint64_t g_si_trace[1024 * kTraceSlots];
+extern "C" hipError_t si_trace_read(void* dst, size_t bytes) {
+  return hipMemcpyFromSymbol(dst, HIP_SYMBOL(g_si_trace), bytes, 0, hipMemcpyDeviceToHost);
+}
+#endif
+
+constexpr int kLayerWaves = 12;
 constexpr int kLayerThreads = kLayerWaves * kWave;
 constexpr int kLayerMaxB = 2;  // larger batches take the two-kernel path (register budget)
-constexpr int kGateWaves = 7;  // waves 1..7
-constexpr int kDownWaves = 8;  // waves 8..15
+constexpr int kGateWaves = 7;  // waves 1..7: gate/up; wave 0: decisions and compaction
+constexpr int kDownWaves = 4;  // waves 8..11: down-projection
 constexpr int kMaxSignUnitsPerWave = kMaxD / 128 / kLayerWaves;  // 4
 constexpr long kPollLimit = 1l << 16;
 constexpr uint32_t kNoAS = 1u, kNoSpec = 2u;
@@ -61,10 +70,10 @@ struct LayerArgs {
   int32_t* n_out;
   uint32_t* hdr;
   uint64_t* status;  // [groups] look-back words
-  uint64_t* lhdr;    // [groups] tag | kept count
-  uint64_t* lent;    // [groups][64] tag | conf << 31 | row
-  uint64_t* h3e;     // [groups][64][B] tag | fp32 bits
+  uint64_t* lmask;   // [groups][4] tag | kept mask low/high half, tag | confident mask low/high half
+  uint64_t* h3e;     // [groups][64][B] tag | fp32 bits, by rank in the group's kept list
   uint64_t* zflag;   // [tiles] tag once the tile of y is zero
+  uint32_t* ready;   // [2 parities][2][groups]: per chunk, groups whose masks / h3 are published
   int32_t* counts;   // [groups][2] W_up rows read, W_down^T rows read (tile-0 items)
   float* y;
   int tiles, chunks, gpc;
@@ -91,6 +100,16 @@ __device__ inline uint32_t poll_lane(const uint64_t* p, bool active, uint32_t ta
       if (++spins > kPollLimit) {
         abort = true;
         if (pending) atomicOr(&hdr[H_ERR], kErrLookbackSpin);
+#ifdef SI_TRACE
+        if (pending) {  // block, wave, word index, last seen tag, expected tag
+          const uint64_t v = ld_agent64(p);
+          g_si_trace[(size_t)blockIdx.x * kTraceSlots + 26] = blockIdx.x;
+          g_si_trace[(size_t)blockIdx.x * kTraceSlots + 27] = threadIdx.x >> 6;
+          g_si_trace[(size_t)blockIdx.x * kTraceSlots + 28] = (uint64_t)(size_t)p;
+          g_si_trace[(size_t)blockIdx.x * kTraceSlots + 29] = v >> 32;
+          g_si_trace[(size_t)blockIdx.x * kTraceSlots + 30] = tag;
+        }
+#endif
       } else {
         __builtin_amdgcn_s_sleep(1);
       }
@@ -137,6 +156,38 @@ __device__ inline void poll_batch(const uint64_t* base, const uint32_t (&off)[N]
   }
 }
 
+// Index of the n-th (0-based) set bit of m; m must have more than n bits set.
+__device__ inline int nth_set_bit(uint64_t m, int n) {
+  int pos = 0;
+#pragma unroll
+  for (int s = 32; s >= 1; s >>= 1) {
+    const uint64_t low = m & ((1ull << s) - 1ull);
+    const int c = __popcll(low);
+    if (n >= c) {
+      n -= c;
+      m >>= s;
+      pos += s;
+    } else {
+      m = low;
+    }
+  }
+  return pos;
+}
+
+// Wait until a readiness counter reaches `target` (one lane polls).
+__device__ inline void wait_count(const uint32_t* p, uint32_t target, uint32_t* hdr, bool& abort) {
+  if (abort) return;
+  long spins = 0;
+  while (ld_agent(p) < target) {
+    if (++spins > kPollLimit) {
+      abort = true;
+      atomicOr(&hdr[H_ERR], kErrLookbackSpin);
+      return;
+    }
+    __builtin_amdgcn_s_sleep(4);
+  }
+}
+
 // Wave-wide look-back over the groups' posted counts (see predict.hip).
 __device__ int layer_lookback(const uint64_t* status, int v, uint32_t tag, int lane, uint32_t* hdr) {
   int excl = 0;
@@ -174,102 +225,150 @@ __device__ int layer_lookback(const uint64_t* status, int v, uint32_t tag, int l
 // Gate/up of one kept row; `spec` requests the W_up row together with the
 // W_gate row.  Returns h3 for the B tokens (in every lane) and whether the
 // W_up row was read.
+// Kept rows of a chunk of consecutive groups, as published by the groups'
+// mask words.  Lane l < ng describes group g0 + l.
+struct ChunkView {
+  int g0, ng, E;    // first group, groups, kept rows of the chunk
+  int pre_l;        // inclusive prefix of the kept counts up to this lane's group
+  uint64_t kept_l;  // kept mask of this lane's group
+  uint64_t conf_l;  // confident mask of this lane's group
+};
+
+__device__ inline ChunkView load_chunk(const uint64_t* lmask, int chunk, int gpc, int groups, uint32_t tag,
+                                       uint32_t* hdr, bool& abort, int lane) {
+  ChunkView c;
+  c.g0 = chunk * gpc;
+  c.ng = max(0, min(c.g0 + gpc, groups) - c.g0);
+  const bool mw = lane < 4 * c.ng;
+  const uint32_t mword = poll_lane(&lmask[(size_t)c.g0 * 4 + (mw ? lane : 0)], mw, tag, hdr, abort);
+  const int gl = lane < c.ng ? lane : 0;
+  c.kept_l = (uint64_t)__shfl(mword, 4 * gl, kWave) | ((uint64_t)__shfl(mword, 4 * gl + 1, kWave) << 32);
+  c.conf_l = (uint64_t)__shfl(mword, 4 * gl + 2, kWave) | ((uint64_t)__shfl(mword, 4 * gl + 3, kWave) << 32);
+  int pre = lane < c.ng ? __popcll(c.kept_l) : 0;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const int v = __shfl_up(pre, o, kWave);
+    if (lane >= o) pre += v;
+  }
+  c.pre_l = pre;
+  const int last = __shfl(pre, c.ng > 0 ? c.ng - 1 : 0, kWave);
+  c.E = c.ng > 0 ? last : 0;
+  return c;
+}
+
+// Entry (conf << 31 | row) at position p (< E) of the chunk's kept list; p
+// may differ between lanes.  All lanes must call it.
+__device__ inline uint32_t chunk_entry(const ChunkView& c, int p) {
+  int gi = 0;
+  for (int gg = 0; gg < c.ng; ++gg) gi += (__shfl(c.pre_l, gg, kWave) <= p) ? 1 : 0;
+  gi = min(gi, max(c.ng - 1, 0));
+  // every lane takes part in the shuffles: reading an inactive lane yields 0
+  const int pre_before = __shfl(c.pre_l, gi > 0 ? gi - 1 : 0, kWave);
+  const int li = p - (gi > 0 ? pre_before : 0);
+  const uint64_t km = __shfl(c.kept_l, gi, kWave);
+  const uint64_t cm = __shfl(c.conf_l, gi, kWave);
+  const int bit = (li >= 0 && li < __popcll(km)) ? nth_set_bit(km, li) : 0;
+  return (uint32_t)((c.g0 + gi) * kRowGroup + bit) | (((cm >> bit) & 1ull) ? 0x80000000u : 0u);
+}
+
+// Gate/up of up to R kept rows at once (all their row requests in flight
+// together).  Row r is valid for r < n.  spec[r] requests the W_up row with
+// the W_gate row.  Returns h3 per row and token (in every lane) and whether
+// the W_up row was read.
+template <int B, int NU, int R>
+__device__ inline void gate_up_rows(const u32x4* __restrict__ wg, const u32x4* __restrict__ wu,
+                                    const int (&row)[R], const bool (&spec)[R], int n, int U, const u32x4* xs,
+                                    int lane, bool no_as, float (&h)[R][B], bool (&up)[R]) {
+  u32x4 a[R][NU], c[R][NU];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (r < n) {
+      const u32x4* gr = wg + (size_t)row[r] * U;
+#pragma unroll
+      for (int j = 0; j < NU; ++j) {
+        const int u = lane + kWave * j;
+        if (u < U) a[r][j] = load_nt(gr + u);
+      }
+      if (spec[r]) {
+        const u32x4* ur = wu + (size_t)row[r] * U;
+#pragma unroll
+        for (int j = 0; j < NU; ++j) {
+          const int u = lane + kWave * j;
+          if (u < U) c[r][j] = load_nt(ur + u);
+        }
+      }
+    }
+  }
+  float g[R][B];
+  bool need[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+#pragma unroll
+    for (int t = 0; t < B; ++t) g[r][t] = 0.f;
+    need[r] = false;
+    if (r < n) {
+#pragma unroll
+      for (int j = 0; j < NU; ++j) {
+        const int u = lane + kWave * j;
+        if (u < U) {
+#pragma unroll
+          for (int t = 0; t < B; ++t) g[r][t] = dot8(a[r][j], xs[t * U + u], g[r][t]);
+        }
+      }
+      bool any = false;
+#pragma unroll
+      for (int t = 0; t < B; ++t) {
+        g[r][t] = fmaxf(wave_sum(g[r][t]), 0.f);
+        any |= g[r][t] > 0.f;
+      }
+      need[r] = any || no_as;
+      up[r] = need[r] || spec[r];
+      // late W_up request where the gate value asks for it
+      if (need[r] && !spec[r]) {
+        const u32x4* ur = wu + (size_t)row[r] * U;
+#pragma unroll
+        for (int j = 0; j < NU; ++j) {
+          const int u = lane + kWave * j;
+          if (u < U) c[r][j] = load_nt(ur + u);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+#pragma unroll
+    for (int t = 0; t < B; ++t) h[r][t] = 0.f;
+    if (r < n && need[r]) {
+      float uu[B];
+#pragma unroll
+      for (int t = 0; t < B; ++t) uu[t] = 0.f;
+#pragma unroll
+      for (int j = 0; j < NU; ++j) {
+        const int u = lane + kWave * j;
+        if (u < U) {
+#pragma unroll
+          for (int t = 0; t < B; ++t) uu[t] = dot8(c[r][j], xs[t * U + u], uu[t]);
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < B; ++t) h[r][t] = g[r][t] * wave_sum(uu[t]);
+    }
+  }
+}
+
+// Rows handled together by one gate/up wave (bounded by registers).
 template <int B, int NU>
-__device__ inline bool gate_up_spec(const u32x4* __restrict__ wg, const u32x4* __restrict__ wu, int row, int U,
-                                    const u32x4* xs, int lane, bool spec, bool no_as, float (&h)[B]) {
-  constexpr int J = NU;                     // 16-byte units per lane
-  constexpr int JC = NU <= 10 ? NU : 1;     // both rows in registers only up to d = 5120
-  const u32x4* gr = wg + (size_t)row * U;
-  const u32x4* ur = wu + (size_t)row * U;
-  const bool two = spec && NU <= 10;
-  u32x4 a[J], c[JC];
-#pragma unroll
-  for (int j = 0; j < J; ++j) {
-    const int u = lane + kWave * j;
-    if (u < U) a[j] = load_nt(gr + u);
-  }
-  if (two) {
-#pragma unroll
-    for (int j = 0; j < JC; ++j) {
-      const int u = lane + kWave * j;
-      if (u < U) c[j] = load_nt(ur + u);
-    }
-  }
-  float g[B];
-#pragma unroll
-  for (int t = 0; t < B; ++t) g[t] = 0.f;
-#pragma unroll
-  for (int j = 0; j < J; ++j) {
-    const int u = lane + kWave * j;
-    if (u < U) {
-#pragma unroll
-      for (int t = 0; t < B; ++t) g[t] = dot8(a[j], xs[t * U + u], g[t]);
-    }
-  }
-  bool any = false;
-#pragma unroll
-  for (int t = 0; t < B; ++t) {
-    g[t] = fmaxf(wave_sum(g[t]), 0.f);
-    any |= g[t] > 0.f;
-  }
-#pragma unroll
-  for (int t = 0; t < B; ++t) h[t] = 0.f;
-  const bool up = any || no_as || two;
-  if (any || no_as) {
-    float u[B];
-#pragma unroll
-    for (int t = 0; t < B; ++t) u[t] = 0.f;
-    if (two) {
-#pragma unroll
-      for (int j = 0; j < JC; ++j) {
-        const int uu = lane + kWave * j;
-        if (uu < U) {
-#pragma unroll
-          for (int t = 0; t < B; ++t) u[t] = dot8(c[j], xs[t * U + uu], u[t]);
-        }
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < J; ++j) {
-        const int uu = lane + kWave * j;
-        if (uu < U) a[j] = load_nt(ur + uu);
-      }
-#pragma unroll
-      for (int j = 0; j < J; ++j) {
-        const int uu = lane + kWave * j;
-        if (uu < U) {
-#pragma unroll
-          for (int t = 0; t < B; ++t) u[t] = dot8(a[j], xs[t * U + uu], u[t]);
-        }
-      }
-    }
-#pragma unroll
-    for (int t = 0; t < B; ++t) h[t] = g[t] * wave_sum(u[t]);
-  }
-  return up;
-}
-
-// W_down^T segments in flight per down wave (fewer for larger batches to
-// bound the registers holding h3 values).
-template <int B>
-constexpr int down_batch() { return B == 1 ? 8 : 4; }
-
-// Units of 16 bytes per lane that cover a row of d fp16 values (template
-// bucket of the kernel).
-inline int units_per_lane(int d) {
-  const int nu = (d / 8 + kWave - 1) / kWave;
-  return nu <= 1 ? 1 : nu <= 2 ? 2 : nu <= 4 ? 4 : nu <= 8 ? 8 : nu <= 10 ? 10 : 16;
-}
+constexpr int gate_rows_in_flight() { return (B == 1 && NU <= 8) ? 2 : 1; }
 
 template <int B, int NU>
 __global__ __launch_bounds__(kLayerThreads) void k_layer(LayerArgs a) {
-  constexpr int kDownBatch = down_batch<B>();
-  extern __shared__ u32x4 xs[];  // [B][d/8] fp16 tokens
+  constexpr int kDownBatch = kWave / 4;  // entries polled per batch by one down wave (one per lane)
+  extern __shared__ u32x4 xs[];           // [B][d/8] fp16 tokens
   __shared__ __attribute__((aligned(16))) uint32_t xw[B * (kMaxD / 32)];
   __shared__ int cnt[B][kWave];
   __shared__ uint32_t kept[kRowGroup];  // conf << 31 | row
   __shared__ float red[B][kTile];
-  __shared__ int s_nkept, s_up, s_down;
+  __shared__ int s_nkept, s_up, s_down, s_adone;
   __shared__ uint32_t s_epoch;
 
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -279,6 +378,10 @@ __global__ __launch_bounds__(kLayerThreads) void k_layer(LayerArgs a) {
   const bool has_item = g < items;
   const int tile = g % a.tiles, chunk = g / a.tiles;
 
+  if (wv == 0) SI_TRACE_MARK(0);
+#ifdef SI_TRACE
+  if (tid == 0) g_si_trace[(size_t)blockIdx.x * kTraceSlots + 31] = (uint64_t)(size_t)a.h3e;
+#endif
   // ---- packed-sign loads of this group, issued before anything else
   u32x4 sreg[kMaxSignUnitsPerWave];
   const u32x4* sg = a.signs + (size_t)g * units * kRowGroup + lane;
@@ -295,21 +398,28 @@ __global__ __launch_bounds__(kLayerThreads) void k_layer(LayerArgs a) {
   if (tid == 0) {
     s_up = 0;
     s_down = 0;
-    s_epoch = ld_agent(&a.hdr[H_PRED_EPOCH]);
+    s_adone = 0;
+    s_epoch = ld_agent(&a.hdr[H_EPOCH]);
   }
   const bool owns_tile = g < a.tiles;
+  if (g == 0) {
+    // the next call's readiness counters start from zero (this call's were
+    // cleared by the previous call, or by the zero-filled workspace)
+    const uint32_t nxt = (ld_agent(&a.hdr[H_EPOCH]) + 1u) & 1u;
+    for (int i = tid; i < 2 * groups; i += kLayerThreads) a.ready[(size_t)nxt * 2 * groups + i] = 0u;
+  }
   if (owns_tile) {
     for (int i = tid; i < B * kTile; i += kLayerThreads) {
       const int t = i / kTile, col = g * kTile + (i - t * kTile);
-      if (col < d) a.y[(size_t)t * d + col] = 0.f;
+      if (col < d) __hip_atomic_store(&a.y[(size_t)t * d + col], 0.f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    wait_own_stores();
   }
   __syncthreads();
   const uint32_t epoch = s_epoch;
   const uint32_t tag = epoch_tag(epoch);
-  if (owns_tile && tid == 0) {
-    __hip_atomic_store(&a.zflag[g], tagged(tag, 1u), __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-  }
+  if (wv == 0) SI_TRACE_MARK(1);
+  if (owns_tile && tid == 0) st_agent64(&a.zflag[g], tagged(tag, 1u));
   for (int i = tid; i < B * W; i += kLayerThreads) {
     const int t = i / W, w = i - t * W;
     xw[i] = sign_word(&xs[t * U + 4 * w]);
@@ -341,6 +451,7 @@ __global__ __launch_bounds__(kLayerThreads) void k_layer(LayerArgs a) {
     }
   }
   __syncthreads();
+  if (wv == 0) SI_TRACE_MARK(2);
 
   // ---- wave 0: Eq. (2), mask, kept list, publication
   if (wv == 0) {
@@ -357,62 +468,100 @@ __global__ __launch_bounds__(kLayerThreads) void k_layer(LayerArgs a) {
     const uint64_t ballot = __ballot(keep);
     const int nk = __popcll(ballot);
     const int rank = __popcll(ballot & lanes_below(lane));
-    if (keep) {
-      const uint32_t e = (conf ? 0x80000000u : 0u) | (uint32_t)row;
-      kept[rank] = e;
-      st_agent64(&a.lent[(size_t)g * kRowGroup + rank], tagged(tag, e));
+    const uint64_t cballot = __ballot(keep && conf);
+    if (keep) kept[rank] = (conf ? 0x80000000u : 0u) | (uint32_t)row;
+    if (lane < 4) {
+      const uint64_t m = lane < 2 ? ballot : cballot;
+      st_agent64(&a.lmask[(size_t)g * 4 + lane], tagged(tag, (uint32_t)(m >> (32 * (lane & 1)))));
     }
+    wait_own_stores();
     if (lane == 0) {
       s_nkept = nk;
-      st_agent64(&a.lhdr[g], tagged(tag, (uint32_t)nk));
       st_agent64(&a.status[g], tagged(tag, (uint32_t)((g == 0 ? kFlagPrefix : kFlagAggregate) | (uint64_t)nk)));
+      __hip_atomic_fetch_add(&a.ready[(size_t)(epoch & 1u) * 2 * groups + g / a.gpc], 1u, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
     }
   }
   __syncthreads();
+  if (wv == 0) SI_TRACE_MARK(3);
   const int nkept = s_nkept;
   const bool no_as = (a.flags & kNoAS) != 0;
 
   if (wv == 0) {
-    // ---- ordered compaction
+    // ---- ordered compaction: every group posted its count right after
+    // counting, so the look-back completes in a few round trips
     const int excl = g == 0 ? 0 : layer_lookback(a.status, g, tag, lane, a.hdr);
-    if (lane == 0 && g > 0) st_agent64(&a.status[g], tagged(tag, (uint32_t)(kFlagPrefix | (uint64_t)(excl + nkept))));
+    if (lane == 0 && g > 0)
+      st_agent64(&a.status[g], tagged(tag, (uint32_t)(kFlagPrefix | (uint64_t)(excl + nkept))));
     if (lane < nkept && a.idx) a.idx[excl + lane] = (int32_t)(kept[lane] & 0x7fffffffu);
     if (lane == 0 && g == groups - 1) {
       if (a.n_out) *a.n_out = excl + nkept;
-      st_agent(&a.hdr[H_PRED_EPOCH], epoch + 1u);  // every group has posted: all blocks read this epoch
+      st_agent(&a.hdr[H_EPOCH], epoch + 1u);  // every group has posted: all blocks read this epoch
     }
+    SI_TRACE_MARK(4);
+#ifdef SI_TRACE
+    if (lane == 0) g_si_trace[(size_t)blockIdx.x * kTraceSlots + 19] = nkept;
+#endif
   } else if (wv <= kGateWaves) {
-    // ---- gate/up of this group's kept rows
+    // ---- gate/up, balanced inside the chunk of groups this group belongs
+    // to: the chunk's kept rows (concatenated in group order) are split
+    // evenly over its blocks, so a group with many kept rows does not hold
+    // its chunk back.  Waves 1..7 take this block's positions round-robin,
+    // R rows in flight per wave.
+    constexpr int R = gate_rows_in_flight<B, NU>();
+    constexpr int NGW = kGateWaves;
+    bool abort = false;
+    const ChunkView cv = load_chunk(a.lmask, g / a.gpc, a.gpc, groups, tag, a.hdr, abort, lane);
+    const int mine = g - cv.g0;
+    const int p_lo = (int)((long long)cv.E * mine / max(cv.ng, 1));
+    const int p_hi = (int)((long long)cv.E * (mine + 1) / max(cv.ng, 1));
     int n_up = 0;
-    for (int i = wv - 1; i < nkept; i += kGateWaves) {
-      const uint32_t e = kept[i];
-      const int row = (int)(e & 0x7fffffffu);
-      const bool spec = (e >> 31) != 0 && !(a.flags & kNoSpec);
-      float h[B];
-      n_up += gate_up_spec<B, NU>(a.wg, a.wu, row, U, xs, lane, spec, no_as, h) ? 1 : 0;
+    const bool spec_ok = !(a.flags & kNoSpec) && NU <= 10;
+    for (int i0 = p_lo + wv - 1; i0 < p_hi && !abort; i0 += NGW * R) {
+      int rows[R];
+      bool spec[R];
+      int n = 0;
 #pragma unroll
-      for (int t = 0; t < B; ++t)
-        if (lane == t) st_agent64(&a.h3e[((size_t)g * kRowGroup + i) * B + t], tagged(tag, __float_as_uint(h[t])));
+      for (int r = 0; r < R; ++r) {
+        const int i = i0 + NGW * r;
+        const uint32_t e = chunk_entry(cv, i < p_hi ? i : p_lo);
+        rows[r] = (int)(e & 0x7fffffffu);
+        spec[r] = spec_ok && (e >> 31) != 0;
+        if (i < p_hi) n = r + 1;
+      }
+      float h[R][B];
+      bool up[R];
+      gate_up_rows<B, NU, R>(a.wg, a.wu, rows, spec, n, U, xs, lane, no_as, h, up);
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (r < n) {
+          const int i = i0 + NGW * r;
+          n_up += up[r] ? 1 : 0;
+#pragma unroll
+          for (int t = 0; t < B; ++t)
+            if (lane == t)
+              st_agent64(&a.h3e[((size_t)cv.g0 * kRowGroup + i) * B + t], tagged(tag, __float_as_uint(h[r][t])));
+        }
+      }
     }
-    if (lane == 0 && n_up) atomicAdd(&s_up, n_up);
+    wait_own_stores();
+    if (lane == 0) {
+      if (n_up) atomicAdd(&s_up, n_up);
+      if (atomicAdd(&s_adone, 1) == NGW - 1)  // last gate/up wave of the block
+        __hip_atomic_fetch_add(&a.ready[(size_t)(epoch & 1u) * 2 * groups + groups + g / a.gpc], 1u,
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    SI_TRACE_MARK(4 + wv);  // 5 .. 11
   } else if (has_item) {
-    // ---- down-projection of (tile, chunk)
-    const int wb = wv - (1 + kGateWaves);
-    const int g0 = chunk * a.gpc;
-    const int ng = max(0, min(g0 + a.gpc, groups) - g0);
+    // ---- down-projection of (tile, chunk): this wave takes the chunk's list
+    // positions [16 m + 64 j + 16 wb, +16), one entry per lane
+    const int wb = wv - (kLayerWaves - kDownWaves);
     const int unit = tile * (kTile / 8) + lane;  // 16-byte unit of a W_down^T row: 8 columns
     const bool col_ok = unit < U;
     bool abort = false;
-    // kept counts of the chunk's groups (lane l <-> group g0 + l) and their
-    // inclusive prefix: positions of the chunk's concatenated kept list
-    const int cnt_l = (int)poll_lane(&a.lhdr[g0 + (lane < ng ? lane : 0)], lane < ng, tag, a.hdr, abort);
-    int pre_l = cnt_l;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int v = __shfl_up(pre_l, o, kWave);
-      if (lane >= o) pre_l += v;
-    }
-    const int E = ng > 0 ? __shfl(pre_l, ng - 1, kWave) : 0;
+    const ChunkView cv = load_chunk(a.lmask, chunk, a.gpc, groups, tag, a.hdr, abort, lane);
+    const int E = cv.E;
+    if (wb == 0) SI_TRACE_MARK(12);
     float acc[B][8];
 #pragma unroll
     for (int t = 0; t < B; ++t)
@@ -420,50 +569,46 @@ __global__ __launch_bounds__(kLayerThreads) void k_layer(LayerArgs a) {
       for (int q = 0; q < 8; ++q) acc[t][q] = 0.f;
     int n_down = 0;
     const bool spec_ok = !(a.flags & kNoSpec);
-    for (int p0 = wb; p0 < E && !abort; p0 += kDownWaves * kDownBatch) {
-      // list slots of this wave's positions p0 + 8r
-      uint32_t off[kDownBatch];
-      uint32_t want = 0;
-#pragma unroll
-      for (int r = 0; r < kDownBatch; ++r) {
-        const int p = p0 + kDownWaves * r;
-        const int gi = __popcll(__ballot(lane < ng && pre_l <= p));
-        const int before = gi > 0 ? __shfl(pre_l, gi - 1, kWave) : 0;
-        off[r] = (uint32_t)((g0 + gi) * kRowGroup + (p - before));
-        if (p < E) want |= 1u << r;
-      }
-      uint32_t e[kDownBatch][1];
-      poll_batch<kDownBatch, 1>(a.lent, off, want, tag, e, a.hdr, abort);
+    for (int base = wb * kDownBatch; base < E && !abort; base += kDownWaves * kDownBatch) {
+      // lane r < 16 owns list position base + r
+      const int p = base + lane;
+      const bool mine = lane < kDownBatch && p < E;
+      const uint32_t e = chunk_entry(cv, mine ? p : 0);
+      const uint32_t off = (uint32_t)(cv.g0 * kRowGroup + p);  // h3 of position p
+      if (wb == 0 && base == 0) SI_TRACE_MARK(13);
+      const int nb = min(kDownBatch, E - base);
       u32x4 w[kDownBatch];
       uint32_t loaded = 0;
 #pragma unroll
       for (int r = 0; r < kDownBatch; ++r) {
         w[r] = u32x4{0, 0, 0, 0};
-        if (((want >> r) & 1) && !abort) {
-          const int row = (int)(e[r][0] & 0x7fffffffu);
-          if ((unsigned)row < (unsigned)a.k && ((spec_ok && (e[r][0] >> 31)) || no_as)) {
-            if (col_ok) w[r] = load_nt(a.wdt + (size_t)row * U + unit);
-            loaded |= 1u << r;
-          }
+        const uint32_t er = __shfl(e, r, kWave);
+        const int row = (int)(er & 0x7fffffffu);
+        if (r < nb && !abort && (unsigned)row < (unsigned)a.k && ((spec_ok && (er >> 31)) || no_as)) {
+          if (col_ok) w[r] = load_nt(a.wdt + (size_t)row * U + unit);
+          loaded |= 1u << r;
         }
       }
-      uint32_t hb[kDownBatch][B];
-      poll_batch<kDownBatch, B>(a.h3e, off, want, tag, hb, a.hdr, abort);
+      float hl[B];
+#pragma unroll
+      for (int t = 0; t < B; ++t)
+        hl[t] = __uint_as_float(poll_lane(&a.h3e[mine ? (size_t)off * B + t : 0], mine, tag, a.hdr, abort));
+      if (wb == 0 && base == 0) SI_TRACE_MARK(14);
       float hv[kDownBatch][B];
 #pragma unroll
       for (int r = 0; r < kDownBatch; ++r) {
         bool nz = false;
 #pragma unroll
         for (int t = 0; t < B; ++t) {
-          hv[r][t] = ((want >> r) & 1) && !abort ? __uint_as_float(hb[r][t]) : 0.f;
+          const float hr = __shfl(hl[t], r, kWave);
+          hv[r][t] = (r < nb && !abort) ? hr : 0.f;
           nz |= hv[r][t] != 0.f;
         }
-        if (((want >> r) & 1) && !((loaded >> r) & 1) && nz) {
-          const int row = (int)(e[r][0] & 0x7fffffffu);
-          if ((unsigned)row < (unsigned)a.k) {
-            if (col_ok) w[r] = load_nt(a.wdt + (size_t)row * U + unit);
-            loaded |= 1u << r;
-          }
+        const uint32_t er = __shfl(e, r, kWave);
+        const int row = (int)(er & 0x7fffffffu);
+        if (r < nb && !((loaded >> r) & 1) && nz && (unsigned)row < (unsigned)a.k) {
+          if (col_ok) w[r] = load_nt(a.wdt + (size_t)row * U + unit);
+          loaded |= 1u << r;
         }
       }
       n_down += __popc(loaded);
@@ -486,15 +631,16 @@ __global__ __launch_bounds__(kLayerThreads) void k_layer(LayerArgs a) {
           if (acc[t][q] != 0.f) atomicAdd(&red[t][lane * 8 + q], acc[t][q]);
     }
     if (lane == 0 && tile == 0 && n_down) atomicAdd(&s_down, n_down);
+    SI_TRACE_MARK(15 + wb);  // 15 .. 18
   }
   __syncthreads();
+  if (wv == 0) SI_TRACE_MARK(23);
 
   // ---- add the block's tile into y once block `tile` has zeroed it
   if (has_item) {
     if (wv == 0 && lane == 0) {
       long spins = 0;
-      while ((uint32_t)(__hip_atomic_load(&a.zflag[tile], __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) >> 32) !=
-             tag) {
+      while ((uint32_t)(ld_agent64(&a.zflag[tile]) >> 32) != tag) {
         if (++spins > kPollLimit) {
           atomicOr(&a.hdr[H_ERR], kErrLookbackSpin);
           break;
@@ -503,12 +649,14 @@ __global__ __launch_bounds__(kLayerThreads) void k_layer(LayerArgs a) {
       }
     }
     __syncthreads();
+    if (wv == 0) SI_TRACE_MARK(24);
     for (int i = tid; i < B * kTile; i += kLayerThreads) {
       const int t = i / kTile, col = tile * kTile + (i - t * kTile);
       const float v = (&red[0][0])[i];
       if (col < d && v != 0.f) unsafeAtomicAdd(&a.y[(size_t)t * d + col], v);
     }
   }
+  if (wv == 0) SI_TRACE_MARK(25);
   if (tid == 0) {
     a.counts[2 * g] = s_up;
     a.counts[2 * g + 1] = s_down;
@@ -534,6 +682,13 @@ __global__ __launch_bounds__(256) void k_sum_counts(const int32_t* __restrict__ 
     counters[1] = s[0];
     counters[2] = s[1];
   }
+}
+
+// Units of 16 bytes per lane that cover a row of d fp16 values (template
+// bucket of the kernel).
+inline int units_per_lane(int d) {
+  const int nu = (d / 8 + kWave - 1) / kWave;
+  return nu <= 1 ? 1 : nu <= 2 ? 2 : nu <= 4 ? 4 : nu <= 8 ? 8 : nu <= 10 ? 10 : 16;
 }
 
 // Work split of the down-projection: `tiles` column tiles times `chunks`
@@ -621,15 +776,10 @@ static hipError_t layer_b(const uint32_t* signs, const uint16_t* w_gate, const u
   a.n_out = n_out;
   a.hdr = reinterpret_cast<uint32_t*>(base);
   a.status = reinterpret_cast<uint64_t*>(base + L.status);
-  char* lb = base + L.layer;
-  const size_t groups = (size_t)p.groups;
-  a.lhdr = reinterpret_cast<uint64_t*>(lb);
-  lb += align256(groups * 8);
-  a.lent = reinterpret_cast<uint64_t*>(lb);
-  lb += align256(groups * kRowGroup * 8);
-  a.h3e = reinterpret_cast<uint64_t*>(lb);
-  lb += align256(groups * kRowGroup * B * 8);
-  a.zflag = reinterpret_cast<uint64_t*>(lb);
+  a.ready = reinterpret_cast<uint32_t*>(base + L.ready);
+  a.lmask = reinterpret_cast<uint64_t*>(base + L.lmask);
+  a.zflag = reinterpret_cast<uint64_t*>(base + L.zflag);
+  a.h3e = reinterpret_cast<uint64_t*>(base + L.h3e);
   a.counts = reinterpret_cast<int32_t*>(base + L.counts);
   a.y = y;
   a.tiles = p.tiles;

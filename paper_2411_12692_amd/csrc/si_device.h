@@ -17,7 +17,7 @@ constexpr int kTile = 512;      // columns of y handled by one down-projection b
 
 // Header words at the start of the workspace.
 enum : int {
-  H_PRED_EPOCH = 0,   // call counter tagging the predictor's look-back words
+  H_EPOCH = 0,        // call counter: every predictor or layer call advances it once
   H_ERR = 1,          // sticky device-side error bits
   H_N_INTERNAL = 2,   // kept-row count when the list lives in the workspace
   H_WORDS = 64
@@ -28,15 +28,20 @@ constexpr uint32_t kErrRow = 4u;           // kept-row index outside [0, k)
 
 constexpr int kGateUpMaxBlocks = 2048;     // grid cap of the list-driven gate/up kernel
 
-// Workspace layout (byte offsets), identical on host and device.
+// Workspace layout (byte offsets), identical on host and device.  Regions
+// whose size depends on the batch come last, so every other offset is the
+// same for all batch sizes a workspace serves.
 struct WsLayout {
-  size_t status;  // uint64 look-back word per row group
+  size_t status;  // uint64 [groups] look-back words
   size_t counts;  // int32 [slots][2]: rows whose W_up / W_down^T row was read, per block
   size_t idx;     // int32 [k] kept rows (when the caller gives none)
   size_t mask;    // uint8 [k] mask (when the caller gives none)
   size_t upflag;  // uint8 [k] 1 where the W_up row was read
+  size_t ready;   // uint32 [2][2][groups] single-kernel readiness counters (by call parity)
+  size_t lmask;   // uint64 [groups][4] single-kernel kept / confident masks
+  size_t zflag;   // uint64 [64] single-kernel "tile of y zeroed" flags
   size_t h3;      // float [k][b] h3 per row (valid on kept rows)
-  size_t layer;   // single-kernel exchange words: [groups] + [groups][64] + [groups][64][b] + [64] uint64
+  size_t h3e;     // uint64 [groups][64][b] single-kernel h3 exchange words
   size_t total;
 };
 
@@ -57,10 +62,12 @@ __host__ __device__ inline WsLayout ws_layout(int k, int b) {
   L.idx = L.counts + align256((size_t)count_slots(k) * 2 * sizeof(int32_t));
   L.mask = L.idx + align256((size_t)k * sizeof(int32_t));
   L.upflag = L.mask + align256((size_t)k);
-  L.h3 = L.upflag + align256((size_t)k);
-  L.layer = L.h3 + align256((size_t)k * b * sizeof(float));
-  L.total = L.layer + align256(groups * 8) + align256(groups * kRowGroup * 8) +
-            align256(groups * kRowGroup * (size_t)b * 8) + align256(64 * 8);
+  L.ready = L.upflag + align256((size_t)k);
+  L.lmask = L.ready + align256(groups * 4 * sizeof(uint32_t));
+  L.zflag = L.lmask + align256(groups * 4 * sizeof(uint64_t));
+  L.h3 = L.zflag + align256(64 * sizeof(uint64_t));
+  L.h3e = L.h3 + align256((size_t)k * b * sizeof(float));
+  L.total = L.h3e + align256(groups * kRowGroup * (size_t)b * sizeof(uint64_t));
   return L;
 }
 
@@ -107,6 +114,13 @@ __device__ inline uint64_t lanes_below(int lane) {
 // Tag that marks a word as written in the call with this epoch.  The high
 // bit is always set, so a zero-filled workspace never carries a valid tag.
 __device__ inline uint32_t epoch_tag(uint32_t epoch) { return (epoch & 0x7fffffffu) | 0x80000000u; }
+
+// Wait until this wave's outstanding memory operations have completed.  The
+// exchange words are written with agent-scope (write-through) stores, so once
+// they complete they are visible to agent-scope loads from any XCD; a
+// counter bumped afterwards therefore never runs ahead of the data it
+// announces.  (Consumers also check every word's tag.)
+__device__ inline void wait_own_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 __device__ inline uint32_t ld_agent(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -185,5 +199,22 @@ __device__ inline void gate_up_row(const u32x4* __restrict__ wg, const u32x4* __
     if (lane == t) h3row[(size_t)row * B + t] = h[t];
   if (lane == 0) upflag[row] = up ? 1 : 0;
 }
+
+// Optional phase timeline of the single-kernel path (compile with
+// -DSI_TRACE): per block, the 100 MHz real-time counter at numbered points.
+// Off in normal builds, where the marks compile to nothing.
+constexpr int kTraceSlots = 32;
+#ifdef SI_TRACE
+extern __device__ uint64_t g_si_trace[];
+#define SI_TRACE_MARK(slot)                                                                    \
+  do {                                                                                         \
+    if ((threadIdx.x & 63) == 0)                                                               \
+      g_si_trace[(size_t)blockIdx.x * kTraceSlots + (slot)] = __builtin_amdgcn_s_memrealtime(); \
+  } while (0)
+#else
+#define SI_TRACE_MARK(slot) \
+  do {                      \
+  } while (0)
+#endif
 
 }  // namespace si
