@@ -156,6 +156,14 @@ si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint
                         void* stream);
 
 /*
+ * 1 if si_predict_sparse_mlp runs as a single kernel launch for these shapes
+ * on the current device (b <= 2, k <= 61440, and one 1024-thread block with
+ * 96 KB of LDS resident on every compute unit), 0 if it takes the two-launch
+ * path (same results) or the shapes are invalid.  Host-only query.
+ */
+int si_single_launch(int k, int d, int b);
+
+/*
  * The whole per-token MLP path in one call: si_predict followed by
  * si_sparse_mlp, with the same arguments and outputs (mask, active_idx,
  * n_active and counters may each be NULL).  This is the decode hot path.

@@ -39,6 +39,7 @@ SIGNATURES = {
     "si_transpose_down": (_i, [_p, _i, _i, _p, _p]),
     "si_alpha_threshold": (ctypes.c_int32, [_f, _i]),
     "si_workspace_bytes": (_sz, [_i, _i, _i]),
+    "si_single_launch": (_i, [_i, _i, _i]),
     "si_predict": (_i, [_p, _i, _i, _p, _i, _f, _p, _p, _p, _p, _sz, _p]),
     "si_sparse_mlp": (_i, [_p, _p, _p, _i, _i, _p, _i, _p, _p, _p, _p, _p, _sz, _u32, _p, _p]),
     "si_predict_sparse_mlp": (_i, [_p, _p, _p, _p, _i, _i, _p, _i, _f, _p, _p, _p, _p, _p, _sz, _u32,

@@ -86,6 +86,11 @@ size_t si_workspace_bytes(int k, int d, int b) {
   return si::ws_layout(k, b).total;
 }
 
+int si_single_launch(int k, int d, int b) {
+  if (check_kd(k, d) != SI_OK || check_b(b) != SI_OK) return 0;
+  return si::layer_supported(k, d, b) ? 1 : 0;
+}
+
 int32_t si_alpha_threshold(float alpha, int d) {
   if (std::isnan(alpha) || alpha < 0.0f) return -1;
   if (d < 1 || d > (1 << 24)) return -1;

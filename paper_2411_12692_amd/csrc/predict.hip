@@ -75,8 +75,7 @@ __global__ __launch_bounds__(kPredWaves * kWave) void k_rows(
     uint8_t* __restrict__ mask, int32_t* __restrict__ idx, int32_t* __restrict__ n_out,
     uint64_t* __restrict__ status, uint32_t* __restrict__ hdr,
     const u32x4* __restrict__ wg, const u32x4* __restrict__ wu, float* __restrict__ h3row,
-    uint8_t* __restrict__ upflag, int32_t* __restrict__ counts, float* __restrict__ y, uint32_t flags,
-    uint32_t* __restrict__ ready) {
+    uint8_t* __restrict__ upflag, int32_t* __restrict__ counts, float* __restrict__ y, uint32_t flags) {
   extern __shared__ u32x4 xs[];  // [B][d/8] fp16 tokens
   __shared__ __attribute__((aligned(16))) uint32_t xw[B * (kMaxD / 32)];
   __shared__ int cnt[kPredWaves][B][kWave];
@@ -91,10 +90,6 @@ __global__ __launch_bounds__(kPredWaves * kWave) void k_rows(
 
   if (FUSED && v == 0) {  // y is accumulated with atomics by the down-projection kernel
     for (int i = tid; i < B * d; i += NT) y[i] = 0.f;
-  }
-  if (v == 0) {  // this call advances the epoch: clear the single-kernel path's next readiness counters
-    const uint32_t nxt = (ld_agent(&hdr[H_EPOCH]) + 1u) & 1u;
-    for (int i = tid; i < 2 * groups; i += NT) ready[(size_t)nxt * 2 * groups + i] = 0u;
   }
   // 1. tokens -> LDS, then their packed sign words
   for (int i = tid; i < B * U; i += NT) xs[i] = reinterpret_cast<const u32x4*>(x)[i];
@@ -203,7 +198,7 @@ static hipError_t rows_b(const uint32_t* signs, int k, int d, const uint16_t* x,
       reinterpret_cast<uint64_t*>(base + L.status), reinterpret_cast<uint32_t*>(base),
       reinterpret_cast<const u32x4*>(w_gate), reinterpret_cast<const u32x4*>(w_up),
       reinterpret_cast<float*>(base + L.h3), reinterpret_cast<uint8_t*>(base + L.upflag),
-      reinterpret_cast<int32_t*>(base + L.counts), y, flags, reinterpret_cast<uint32_t*>(base + L.ready));
+      reinterpret_cast<int32_t*>(base + L.counts), y, flags);
   return hipGetLastError();
 }
 

@@ -27,6 +27,7 @@ constexpr uint32_t kErrLookbackSpin = 1u;  // a look-back wait hit its spin limi
 constexpr uint32_t kErrRow = 4u;           // kept-row index outside [0, k)
 
 constexpr int kGateUpMaxBlocks = 2048;     // grid cap of the list-driven gate/up kernel
+constexpr int kMaxLayerBlocks = 1024;      // grid cap of the single-kernel path
 
 // Workspace layout (byte offsets), identical on host and device.  Regions
 // whose size depends on the batch come last, so every other offset is the
@@ -37,9 +38,9 @@ struct WsLayout {
   size_t idx;     // int32 [k] kept rows (when the caller gives none)
   size_t mask;    // uint8 [k] mask (when the caller gives none)
   size_t upflag;  // uint8 [k] 1 where the W_up row was read
-  size_t ready;   // uint32 [2][2][groups] single-kernel readiness counters (by call parity)
   size_t lmask;   // uint64 [groups][4] single-kernel kept / confident masks
   size_t zflag;   // uint64 [64] single-kernel "tile of y zeroed" flags
+  size_t alive;   // uint64 [kMaxLayerBlocks] single-kernel words of blocks that own no row group
   size_t h3;      // float [k][b] h3 per row (valid on kept rows)
   size_t h3e;     // uint64 [groups][64][b] single-kernel h3 exchange words
   size_t total;
@@ -62,10 +63,10 @@ __host__ __device__ inline WsLayout ws_layout(int k, int b) {
   L.idx = L.counts + align256((size_t)count_slots(k) * 2 * sizeof(int32_t));
   L.mask = L.idx + align256((size_t)k * sizeof(int32_t));
   L.upflag = L.mask + align256((size_t)k);
-  L.ready = L.upflag + align256((size_t)k);
-  L.lmask = L.ready + align256(groups * 4 * sizeof(uint32_t));
+  L.lmask = L.upflag + align256((size_t)k);
   L.zflag = L.lmask + align256(groups * 4 * sizeof(uint64_t));
-  L.h3 = L.zflag + align256(64 * sizeof(uint64_t));
+  L.alive = L.zflag + align256(64 * sizeof(uint64_t));
+  L.h3 = L.alive + align256(kMaxLayerBlocks * sizeof(uint64_t));
   L.h3e = L.h3 + align256((size_t)k * b * sizeof(float));
   L.total = L.h3e + align256(groups * kRowGroup * (size_t)b * sizeof(uint64_t));
   return L;
@@ -204,15 +205,26 @@ __device__ inline void gate_up_row(const u32x4* __restrict__ wg, const u32x4* __
 // -DSI_TRACE): per block, the 100 MHz real-time counter at numbered points.
 // Off in normal builds, where the marks compile to nothing.
 constexpr int kTraceSlots = 32;
+constexpr int kTraceWaveMarks = 8;
 #ifdef SI_TRACE
 extern __device__ uint64_t g_si_trace[];
+extern __device__ uint64_t g_si_trace_wave[];
 #define SI_TRACE_MARK(slot)                                                                    \
   do {                                                                                         \
     if ((threadIdx.x & 63) == 0)                                                               \
       g_si_trace[(size_t)blockIdx.x * kTraceSlots + (slot)] = __builtin_amdgcn_s_memrealtime(); \
   } while (0)
+#define SI_TRACE_WAVE(mark)                                                                           \
+  do {                                                                                                \
+    if ((threadIdx.x & 63) == 0)                                                                      \
+      g_si_trace_wave[((size_t)blockIdx.x * 16 + (threadIdx.x >> 6)) * kTraceWaveMarks + (mark)] =   \
+          __builtin_amdgcn_s_memrealtime();                                                           \
+  } while (0)
 #else
 #define SI_TRACE_MARK(slot) \
+  do {                      \
+  } while (0)
+#define SI_TRACE_WAVE(mark) \
   do {                      \
   } while (0)
 #endif

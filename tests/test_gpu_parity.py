@@ -93,6 +93,13 @@ def device_errors(ws: torch.Tensor) -> int:
     return int(ws[4:8].view(torch.int32).item())
 
 
+def check_list(idx, n, mask_ref):
+    """The fused call's ascending kept list and count, bit-exact."""
+    nref = int(mask_ref.sum())
+    assert int(n.item()) == nref
+    assert np.array_equal(idx.cpu().numpy()[:nref], oracle.active_rows(mask_ref))
+
+
 def check_mlp(c: Case, x, mask_ref, y, counters=None, flags=0):
     assert device_errors(c.layer.workspace) == 0
     out = oracle.sparse_mlp(c.wg, c.wu, c.wd, x, mask_ref)
@@ -190,6 +197,7 @@ def test_sparse_mlp_tiny_all_alphas(tiny, alpha):
     torch.cuda.synchronize()
     m_ref, _, _ = oracle.predict_rows(tiny.packed, tiny.x, alpha)
     assert np.array_equal(mask.cpu().numpy(), m_ref)
+    check_list(idx, n, m_ref)
     check_mlp(tiny, tiny.x, m_ref, y, cnt)
 
 
@@ -265,19 +273,24 @@ def test_batch_union(b):
         torch.cuda.synchronize()
         m_ref = check_predict(c, c.x, alpha)
         assert np.array_equal(mask.cpu().numpy(), m_ref)
+        check_list(idx, n, m_ref)
         check_mlp(c, c.x, m_ref, y, cnt)
 
 
-@pytest.mark.parametrize("k,d", [(1, 128), (63, 128), (65, 384), (129, 8192), (1000, 640)])
+@pytest.mark.parametrize("k,d", [(1, 128), (63, 128), (65, 384), (129, 8192), (1000, 640), (1, 8192),
+                                 (20000, 384), (61440, 128)])
 def test_sparse_mlp_edge_shapes(k, d):
+    """Ragged tails of rows, pieces and tiles; k = 20000 and 61440 give more
+    64-row groups than there are blocks (several groups per block)."""
     rng = np.random.default_rng(k * 17 + d)
     c = Case(rand_bits(rng, (k, d), False), rand_bits(rng, (k, d), False), rand_bits(rng, (d, k), False),
              rand_bits(rng, (1, d), False))
     for alpha in [1.0, math.inf]:
-        y, (mask, _, _, cnt) = c.layer(to_dev(c.x), alpha, outputs=True)
+        y, (mask, idx, n, cnt) = c.layer(to_dev(c.x), alpha, outputs=True)
         torch.cuda.synchronize()
         m_ref = oracle.predict_rows(c.packed, c.x, alpha)[0]
         assert np.array_equal(mask.cpu().numpy(), m_ref)
+        check_list(idx, n, m_ref)
         if m_ref.any():
             check_mlp(c, c.x, m_ref, y, cnt)
 
@@ -298,6 +311,7 @@ def test_7b_layer(l7b, alpha):
     torch.cuda.synchronize()
     m_ref = check_predict(l7b, l7b.x, alpha)
     assert np.array_equal(mask.cpu().numpy(), m_ref)
+    check_list(idx, n, m_ref)
     check_mlp(l7b, l7b.x, m_ref, y, cnt)
 
 
@@ -308,7 +322,18 @@ def test_13b_layer():
     torch.cuda.synchronize()
     m_ref = check_predict(c, c.x, 1.0)
     assert np.array_equal(mask.cpu().numpy(), m_ref)
+    check_list(idx, n, m_ref)
     check_mlp(c, c.x, m_ref, y, cnt)
+
+
+@pytest.mark.parametrize("k,d,b,one", [(11008, 4096, 1, 1), (13824, 5120, 1, 1), (1376, 512, 1, 1),
+                                       (11008, 4096, 2, 1), (1, 128, 1, 1), (61440, 128, 1, 1),
+                                       (61441, 128, 1, 0), (11008, 4096, 3, 0), (11008, 4096, 9, 0)])
+def test_single_launch_path(k, d, b, one):
+    """The shapes the parity tests use at b <= 2 run the one-launch kernel
+    (so its results are the ones checked); larger batches and k take the
+    two-launch path."""
+    assert si._lib.load().si_single_launch(k, d, b) == one
 
 
 @pytest.mark.parametrize("flags", [0, si.SI_NO_SPECULATION])
