@@ -94,6 +94,7 @@ struct LayerArgs {
   int32_t* counts;  // [blocks][2] W_up rows read, W_down^T rows read (tile-0 items)
   float* y;
   int groups, tiles, chunks;
+  double inv_blocks, inv_chunks;  // 1 / grid size, 1 / chunks (exact floors of n b / P, n c / C)
 };
 
 // Everything the block keeps in LDS, carved from the dynamic allocation.
@@ -108,8 +109,9 @@ struct LayerLds {
   uint32_t xw[B * kMaxD / 32];          // sign words of the tokens
   int cpart[kLWaves][B][kWave];         // per-wave N_neg partial counts of the current group
   uint32_t pm[4 * kMaxLayerGroups];     // published masks of every group
-  int pre[kMaxLayerGroups];             // inclusive prefix of the kept counts
   int wtot[kLWaves];
+  int pre[kMaxLayerGroups];             // inclusive prefix of the kept counts
+  int gfirst[2];                        // group holding the first position of the slice / the down item
   float dots[kRoundRows][2][B];         // W_gate . x and W_up . x of the round's rows
   float h1[kRoundRows][B];
   uint32_t need[kRoundRows];            // round row needs a late W_up read
@@ -143,6 +145,23 @@ __device__ inline float wave_total(float v) {
 }
 
 __device__ inline int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+template <int CTRL, int ROWS>
+__device__ inline int dpp_get(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xF, true);
+}
+
+// Inclusive prefix sum over the 64 lanes: shifts by 1, 2, 4, 8 inside each
+// row of 16 lanes, then the last lane of rows 0 and 1 broadcast forward.
+__device__ inline int wave_incl_scan(int v) {
+  v += dpp_get<0x111, 0xF>(v);  // row_shr:1
+  v += dpp_get<0x112, 0xF>(v);  // row_shr:2
+  v += dpp_get<0x114, 0xF>(v);  // row_shr:4
+  v += dpp_get<0x118, 0xF>(v);  // row_shr:8
+  v += dpp_get<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+  v += dpp_get<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
+  return v;
+}
 
 // Poll one tagged word per lane (lanes may use different addresses) until it
 // carries `tag`; returns the payload.  After the spin limit the wave stops
@@ -364,62 +383,68 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
   }
   SI_TRACE_MARK(3);
 
-  // ---- inclusive prefix of the kept counts (one group per thread)
-  {
-    int c = 0;
-    if (tid < G) c = __popc(L.pm[4 * tid]) + __popc(L.pm[4 * tid + 1]);
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int v = __shfl_up(c, o, kWave);
-      if (lane >= o) c += v;
-    }
-    if (lane == kWave - 1) L.wtot[wv] = c;
-    __syncthreads();
-    if (wv * kWave < G) {
-      int off = 0;
-      for (int w = 0; w < wv; ++w) off += L.wtot[w];
-      if (tid < G) L.pre[tid] = c + off;
-    }
-    __syncthreads();
-  }
+  // ---- plan: kept count of every group (one group per thread) and their
+  // block-wide prefix; the block's gate/up slice and down item; then one
+  // wave per group that holds positions of them writes their list entries
+  // (lane = row: rank among the group's kept rows)
   const int C = a.chunks;
   const bool has_item = blk < T * C;
   const int tile = has_item ? blk % T : 0, chunk = has_item ? blk / T : 0;
-  if (tid == 0) {  // block scalars, once
-    const int n = L.pre[G - 1];
-    L.sc[0] = n;
-    L.sc[1] = (int)((unsigned)n * (unsigned)blk / (unsigned)P);
-    L.sc[2] = (int)((unsigned)n * (unsigned)(blk + 1) / (unsigned)P);
-    L.sc[3] = has_item ? (int)((unsigned)n * (unsigned)chunk / (unsigned)C) : 0;
-    L.sc[4] = has_item ? (int)((unsigned)n * (unsigned)(chunk + 1) / (unsigned)C) : 0;
-    if (blk == 0) *a.n_out = n;
-  }
-  __syncthreads();
-  const int lo = uniform(L.sc[1]), hi = uniform(L.sc[2]);
-  const int dlo = uniform(L.sc[3]), dhi = uniform(L.sc[4]);
-
-  // ---- list entries of the block's positions: the thread of each group
-  // walks its kept rows and writes those that fall in the block's gate/up
-  // slice (and the kept list there) or in its down item
-  if (tid < G) {
-    const uint64_t km = (uint64_t)L.pm[4 * tid] | ((uint64_t)L.pm[4 * tid + 1] << 32);
-    const uint64_t cm = (uint64_t)L.pm[4 * tid + 2] | ((uint64_t)L.pm[4 * tid + 3] << 32);
-    const int pe = L.pre[tid] - __popcll(km);  // list position of the group's first kept row
-    const int pi = L.pre[tid];
-    if ((pe < hi && pi > lo) || (pe < dhi && pi > dlo)) {
-      uint64_t m = km;
-      for (int p = pe; m; ++p, m &= m - 1) {
-        const int bit = __builtin_ctzll(m);
-        const uint32_t e = (uint32_t)(tid * kRowGroup + bit) | (((cm >> bit) & 1ull) ? 0x80000000u : 0u);
-        if (p >= lo && p < hi) {
-          L.srow[p - lo] = e;
-          a.idx[p] = tid * kRowGroup + bit;
+  {
+    uint64_t km = 0;
+    if (tid < G) km = (uint64_t)L.pm[4 * tid] | ((uint64_t)L.pm[4 * tid + 1] << 32);
+    const int c = __popcll(km);
+    const int incl = wave_incl_scan(c);
+    if (lane == kWave - 1) L.wtot[wv] = incl;
+    if (tid < 2) L.gfirst[tid] = G;
+    __syncthreads();
+    const int wt = wave_incl_scan(lane < kLWaves ? L.wtot[lane] : 0);  // lanes 0..15: prefix of wave totals
+    const int n = uniform(__builtin_amdgcn_readlane(wt, kLWaves - 1));
+    const int before = wv > 0 ? uniform(__builtin_amdgcn_readlane(wt, wv > 0 ? wv - 1 : 0)) : 0;
+    // floor(n b / P) etc.: (x + 1/2) / P is at least 1 / (2P) away from an integer
+    const int lo_ = (int)(((double)n * blk + 0.5) * a.inv_blocks);
+    const int hi_ = (int)(((double)n * (blk + 1) + 0.5) * a.inv_blocks);
+    const int dlo_ = has_item ? (int)(((double)n * chunk + 0.5) * a.inv_chunks) : 0;
+    const int dhi_ = has_item ? (int)(((double)n * (chunk + 1) + 0.5) * a.inv_chunks) : 0;
+    const int pi = before + incl, pe = pi - c;  // the group's kept rows hold positions [pe, pi)
+    if (tid < G) {
+      L.pre[tid] = pi;
+      if (lo_ < hi_ && pe <= lo_ && lo_ < pi) L.gfirst[0] = tid;
+      if (dlo_ < dhi_ && pe <= dlo_ && dlo_ < pi) L.gfirst[1] = tid;
+    }
+    if (tid == 0) {
+      L.sc[1] = lo_;
+      L.sc[2] = hi_;
+      L.sc[3] = dlo_;
+      L.sc[4] = dhi_;
+      if (blk == 0) *a.n_out = n;
+    }
+    __syncthreads();
+    // waves 0..7: groups from the slice's first; waves 8..15: from the down item's first
+    const bool down_side = wv >= kLWaves / 2;
+    const int rlo = down_side ? dlo_ : lo_, rhi = down_side ? dhi_ : hi_;
+    for (int g = uniform(L.gfirst[down_side ? 1 : 0]) + (wv & 7); g < G; g += kLWaves / 2) {
+      const int gpi = L.pre[g];
+      const uint64_t gk = (uint64_t)L.pm[4 * g] | ((uint64_t)L.pm[4 * g + 1] << 32);
+      const int gpe = gpi - __popcll(gk);
+      if (gpe >= rhi) break;
+      if (gpi <= rlo) continue;
+      const uint64_t gc = (uint64_t)L.pm[4 * g + 2] | ((uint64_t)L.pm[4 * g + 3] << 32);
+      const int q = gpe + __popcll(gk & lanes_below(lane));
+      if (((gk >> lane) & 1ull) && q >= rlo && q < rhi) {
+        const uint32_t e = (uint32_t)(g * kRowGroup + lane) | (((gc >> lane) & 1ull) ? 0x80000000u : 0u);
+        if (down_side) {
+          L.dent[q - rlo] = e;
+        } else {
+          L.srow[q - rlo] = e;
+          a.idx[q] = g * kRowGroup + lane;
         }
-        if (p >= dlo && p < dhi) L.dent[p - dlo] = e;
       }
     }
   }
   __syncthreads();
+  const int lo = uniform(L.sc[1]), hi = uniform(L.sc[2]);
+  const int dlo = uniform(L.sc[3]), dhi = uniform(L.sc[4]);
   SI_TRACE_MARK(4);
 
   // ---- down requests of a round: this wave's positions q0 + wv + 16 j
@@ -735,6 +760,8 @@ static hipError_t layer_b(const uint32_t* signs, const uint16_t* w_gate, const u
   a.groups = row_groups(k);
   a.tiles = (d + kTile - 1) / kTile;
   a.chunks = P / a.tiles;
+  a.inv_blocks = 1.0 / P;
+  a.inv_chunks = 1.0 / a.chunks;
   k_layer<B, NU><<<P, kLThreads, kLayerLdsBytes, s>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !counters) return e;
