@@ -482,8 +482,6 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
       active = imat == 0 || (spec_ok && (e >> 31));
       if (active) load_row<NU>((imat ? a.wu : a.wg) + (size_t)(e & 0x7fffffffu) * U, U, lane, v);
     }
-    if (first && dlo < dhi) issue_down(dlo);  // overlaps the gate/up traffic
-    first = false;
     SI_TRACE_WAVE(0);
     if (active) {
       float dt[B];
@@ -494,6 +492,10 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
       }
     }
     SI_TRACE_WAVE(1);
+    // the down item's W_down^T pieces go out once this wave's gate/up data is
+    // in, so they stream behind the loads that h3 depends on
+    if (first && dlo < dhi) issue_down(dlo);
+    first = false;
     __syncthreads();
     if (wv == 0) {  // rows of the round: one per lane (mr <= 8)
       bool any = no_as, spec = false;
