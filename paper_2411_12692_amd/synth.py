@@ -174,3 +174,24 @@ def stack_noise(d: int, b: int, config: int, layer: int, token: int, device="cpu
     """Fresh ``N(0, 1)`` noise ``[b][d]`` float32 for one (layer, token)."""
     g = generator(config, layer * 1_000_003 + token, "noise", device)
     return torch.randn(b, d, generator=g, device=device)
+
+
+def stack_input(y_prev, d: int, b: int, config: int, layer: int, token: int, device="cpu") -> torch.Tensor:
+    """Input ``[b][d]`` fp16 of layer ``layer`` of a planted stack at decode
+    step ``token``.
+
+    The magnitudes come from the previous layer's output, normalised to unit
+    RMS, plus fresh ``N(0, 1)`` noise (``|noise|`` alone for layer 0); the
+    signs are the layer's reference pattern, which its gate rows are planted
+    against, so each layer keeps its planted active set for every token.
+    This is harness glue between stacked MLP blocks, not part of the method.
+    """
+    eps = stack_noise(d, b, config, layer, token, device)
+    if y_prev is None:
+        mag = eps.abs()
+    else:
+        y = y_prev.float().reshape(b, d)
+        rms = y.pow(2).mean(dim=-1, keepdim=True).sqrt().clamp_min(1e-30)
+        mag = (y / rms + eps).abs()
+    neg = reference_signs(d, config, layer, device)
+    return fp16_with_sign(mag, neg[None, :].expand(b, d))
