@@ -156,10 +156,11 @@ si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint
                         void* stream);
 
 /*
- * 1 if si_predict_sparse_mlp runs as a single kernel launch for these shapes
- * on the current device (b <= 2, k <= 61440, and one 1024-thread block with
- * 96 KB of LDS resident on every compute unit), 0 if it takes the two-launch
- * path (same results) or the shapes are invalid.  Host-only query.
+ * 1 if si_predict, si_sparse_mlp and si_predict_sparse_mlp run as a single
+ * kernel launch for these shapes on the current device: k <= 61440, b <= 8
+ * (b <= 4 when d > 5120), and one 1024-thread block with 96-160 KB of LDS
+ * resident on every compute unit; 0 if they take the multi-launch path (same
+ * results) or the shapes are invalid.  Host-only query.
  */
 int si_single_launch(int k, int d, int b);
 

@@ -145,6 +145,22 @@ si_status si_predict(const uint32_t* signs, int k, int d, const uint16_t* x, int
   if (std::isnan(alpha) || alpha < 0.0f) return fail(SI_ERR_ALPHA, "alpha=%g must be >= 0 (or +inf)", (double)alpha);
   if (si_status s = check_ws(workspace, workspace_bytes, k, b)) return s;
   const int T = si_alpha_threshold(alpha, d);
+  if (si::layer_supported(k, d, b)) {
+    const si::WsLayout L = si::ws_layout(k, b);
+    char* base = static_cast<char*>(workspace);
+    si::LayerCall c;
+    c.signs = signs;
+    c.x = x;
+    c.k = k;
+    c.d = d;
+    c.b = b;
+    c.T = T;
+    c.mask = mask;
+    c.idx = active_idx ? active_idx : reinterpret_cast<int32_t*>(base + L.idx);
+    c.n_out = n_active ? n_active : reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;
+    c.ws = workspace;
+    return hip_status(si::launch_layer(c, (hipStream_t)stream), "predict launch");
+  }
   return hip_status(si::launch_predict(signs, k, d, x, b, T, mask, active_idx, n_active, workspace,
                                        (hipStream_t)stream),
                     "predict launch");
@@ -178,6 +194,29 @@ si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint
   hipStream_t st = (hipStream_t)stream;
   const si::WsLayout L = si::ws_layout(k, b);
   char* base = static_cast<char*>(workspace);
+  if (si::layer_supported(k, d, b)) {
+    si::LayerCall c;
+    c.w_gate = w_gate;
+    c.w_up = w_up;
+    c.w_down_t = w_down_t;
+    c.x = x;
+    c.k = k;
+    c.d = d;
+    c.b = b;
+    c.flags = flags;
+    if (active_idx) {
+      c.idx_in = active_idx;
+      c.n_in = n_active;
+    } else {
+      c.mask_in = mask;
+      c.idx = reinterpret_cast<int32_t*>(base + L.idx);
+      c.n_out = reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;
+    }
+    c.y = y;
+    c.ws = workspace;
+    c.counters = counters;
+    return hip_status(si::launch_layer(c, st), "sparse_mlp launch");
+  }
   if (!active_idx) {
     int32_t* idx = reinterpret_cast<int32_t*>(base + L.idx);
     int32_t* n = reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;
@@ -223,10 +262,25 @@ si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, c
   hipStream_t st = (hipStream_t)stream;
   const int T = si_alpha_threshold(alpha, d);
   if (si::layer_supported(k, d, b)) {
-    // rows with N_neg < T - d/16 are treated as surely active (speculative W_up / W_down^T requests)
-    return hip_status(si::launch_layer(signs, w_gate, w_up, w_down_t, k, d, x, b, T, d / 16, mask, active_idx,
-                                       n_active, y, workspace, flags, counters, st),
-                      "layer launch");
+    si::LayerCall c;
+    c.signs = signs;
+    c.w_gate = w_gate;
+    c.w_up = w_up;
+    c.w_down_t = w_down_t;
+    c.x = x;
+    c.k = k;
+    c.d = d;
+    c.b = b;
+    c.T = T;
+    c.margin = d / 16;  // rows with N_neg < T - d/16 are treated as surely kept (speculative W_up / W_down^T requests)
+    c.flags = flags;
+    c.mask = mask;
+    c.idx = active_idx;
+    c.n_out = n_active;
+    c.y = y;
+    c.ws = workspace;
+    c.counters = counters;
+    return hip_status(si::launch_layer(c, st), "layer launch");
   }
   if (si_status s = hip_status(si::launch_predict_gate_up(signs, w_gate, w_up, k, d, x, b, T, mask, active_idx,
                                                           n_active, y, workspace, flags, st),

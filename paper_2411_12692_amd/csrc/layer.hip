@@ -1,47 +1,57 @@
-// The whole per-token MLP path of one layer in a single kernel: sign-bit
+// The per-token MLP path of one layer in a single kernel: sign-bit
 // prediction (Section IV-A, Eq. (2)), the ordered list of kept rows, sparse
 // gate/up with actual sparsity and the sparse down-projection (Section IV-B
-// 3)-4)).
+// 3)-4)), for decode batches of up to 8 tokens.  The same kernel serves the
+// three calls of the boundary:
+//
+//  predict mode  the kept rows come from the packed signs (Eq. (2));
+//  mask mode     they come from a caller's mask;
+//  list mode     they come from a caller's ascending list and count;
+//
+// and, with the MLP switched off, the predictor alone.
 //
 // One block of 16 wavefronts per compute unit, all blocks resident at once
-// (the host takes this path only when they fit; each block asks for enough
-// LDS that no two share a CU).
+// (the host takes this path only when they fit; each block asks for more
+// than half of a CU's LDS so that no two share a CU).
 //
-//  1. predict   block b counts N_neg for the 64-row groups b, b+P, ...
-//               (lane per row, the group's units split over the waves),
-//               applies Eq. (2) as N_neg < T, writes the mask and publishes
-//               the group's kept mask and "confident" mask (N_neg < T -
-//               margin: almost surely active) as four tagged words.
+//  1. predict   block b takes the 64-row groups b, b+P, ...: each wave
+//               XOR/popcounts its share of the group's 16-byte units (lane =
+//               row), wave 0 applies Eq. (2) as N_neg < T, writes the mask
+//               and publishes the group's kept mask and "confident" mask
+//               (N_neg < T - margin: almost surely active) as tagged words.
+//               In mask mode the kept mask is read from the caller's mask
+//               and every kept row counts as confident.
 //  2. exchange  every block reads the published masks of all groups (one
-//               poll per word, all in flight together) and forms the same
-//               inclusive prefix of kept counts in LDS, so every block knows
-//               the whole ascending list of kept rows without a serial scan.
-//  3. gate/up   block b takes positions [n b / P, n (b+1) / P) of the list,
-//               an even share whatever the groups' kept counts.  Each row is
-//               cut into 1 KB pieces (one 16-byte unit per lane) dealt to
-//               the 16 waves, so all of the block's row requests are in
-//               flight together.  W_up pieces of confident rows are
-//               requested with the W_gate pieces; other rows read W_up only
-//               where some token's ReLU output is positive (actual
-//               sparsity).  h3 is published per list position.
-//  4. down      block b also owns one item (512-column tile of y, chunk of
-//               list positions).  It requests the tile's W_down^T pieces of
-//               the confident rows of its chunk before the gate/up work, so
-//               they stream in together, then collects h3 of its positions,
-//               fetches the remaining rows whose h3 is non-zero, reduces in
-//               LDS and adds the tile into y with fp32 atomics once the
-//               tile's owner has zeroed it in this call (about P / tiles
-//               atomics per element of y).
+//               poll per word, all in flight together) and forms the prefix
+//               of kept counts, so every block knows the whole ascending list
+//               of kept rows without a serial scan.  List mode skips steps 1
+//               and 2: the list is the caller's.
+//  3. plan      block b takes positions [n b / P, n (b+1) / P) of the list
+//               for gate/up (an even share whatever the groups' kept counts)
+//               and one down-projection item: 512-column tile (b mod T) of y
+//               and chunk (b / T) of the list.
+//  4. gate/up   in rounds of 8 rows, wave w owns (row w/2, W_gate or W_up)
+//               and requests all its 16-byte units at once.  W_up rows of
+//               confident rows are requested with W_gate; other rows read
+//               W_up only where some token's ReLU output is positive (actual
+//               sparsity).  h3 is published per list position and token.
+//  5. down      the tile's W_down^T pieces of the item's confident rows are
+//               requested once each wave's gate/up data is in; the item's h3
+//               words are collected, the remaining rows with non-zero h3 are
+//               fetched, the per-wave partial tiles are folded in LDS (plain
+//               stores) and the tile is added into y with fp32 atomics once
+//               the tile's owner has zeroed it in this call.
 //
 // Blocks exchange data through 64-bit words: the high half is this call's
 // tag (the workspace's call counter with the high bit set), the low half the
 // payload.  They are written with agent-scope write-through stores and read
 // with agent-scope loads; a word is valid once it carries the call's tag, so
 // no cache flush or fence is needed and the workspace is never cleared
-// between calls.  Block 0 advances the call counter once it has seen every
-// block's first word (so every block has read the counter).  Every wait is
-// bounded: past a spin limit the block sets an error bit in the workspace
-// header and goes on without the data.
+// between calls.  Block 0 advances the call counter once it has seen a word
+// of this call from every block (its group's masks, or an "alive" word from
+// blocks without a group and in list mode), i.e. once every block has read
+// it.  Every wait is bounded: past a spin limit the block sets an error bit
+// in the workspace header and goes on without the data.
 
 #include "si_device.h"
 #include "si_launch.h"
@@ -61,19 +71,23 @@ extern "C" hipError_t si_trace_wave_read(void* dst, size_t bytes) {
 
 constexpr int kLWaves = 16;
 constexpr int kLThreads = kLWaves * kWave;
-constexpr int kLayerMaxB = 2;       // larger batches take the two-kernel path (register budget)
-constexpr int kMaxSignUnitsPerWave = kMaxD / 128 / kLWaves;  // 4
-constexpr int kMaxLayerGroups = 960;  // masks of every group are held in LDS (k <= 61440)
+constexpr int kMaxSignUnitsPerWave = (kMaxD / 128 + kLWaves - 1) / kLWaves;  // 4
+constexpr int kMaxLayerGroups = 960;       // masks of every group are held in LDS (k <= 61440)
 constexpr int kMaxPollWords = 4 * kLThreads;
 constexpr int kRoundRows = kLWaves / 2;    // gate/up rows per round: one (row, matrix) item per wave
 constexpr int kDN = 4;                     // down pieces in flight per wave
 constexpr int kDownRound = kLWaves * kDN;  // down positions per round
 constexpr int kMaxSlice = 256;             // gate/up positions of one block (at most)
 constexpr int kMaxDownItem = 4096;         // positions of one down item (at most)
-constexpr int kLayerLdsBytes = 96 * 1024;  // per block: more than half of a CU's LDS
+constexpr int kDownPollThreads = 256;      // waves 0..3 collect a round's h3 words
+constexpr int kMinLds = 96 * 1024;         // more than half of a CU's LDS: one block per CU
+constexpr int kMaxLds = 160 * 1024;
 constexpr long kPollLimit = 1l << 16;
 constexpr uint32_t kNoAS = 1u, kNoSpec = 2u;
+constexpr uint32_t kBadRow = 0xffffffffu;  // list entry outside [0, k)
 static_assert(kTile == kWave * 8, "a down tile is one 16-byte unit per lane");
+
+enum : int { kModePredict = 0, kModeMask = 1, kModeList = 2 };
 
 struct LayerArgs {
   const u32x4* signs;
@@ -81,47 +95,66 @@ struct LayerArgs {
   const u32x4* wu;
   const u32x4* wdt;
   const uint16_t* x;
-  int k, d, T, margin;
+  const uint8_t* mask_in;  // mask mode
+  const int32_t* idx_in;   // list mode
+  const int32_t* n_in;     // list mode
+  int k, d, b, T, margin;
   uint32_t flags;
-  uint8_t* mask;
-  int32_t* idx;
-  int32_t* n_out;
+  int mode, mlp;
+  uint8_t* mask;    // predict mode: written
+  int32_t* idx;     // predict and mask modes: written
+  int32_t* n_out;   // predict and mask modes: written
   uint32_t* hdr;
   uint64_t* pub;    // [groups][4] tag | kept mask low/high half, tag | confident mask low/high half
-  uint64_t* alive;  // [blocks] tag, from blocks that own no group
-  uint64_t* h3e;    // [k][B] tag | fp32 bits of h3, by list position
+  uint64_t* h3e;    // [k][b] tag | fp32 bits of h3, by list position and token
   uint64_t* zflag;  // [tiles] tag once the tile of y is zero
+  uint64_t* alive;  // [blocks] tag, from blocks that publish no group (all blocks in list mode)
   int32_t* counts;  // [blocks][2] W_up rows read, W_down^T rows read (tile-0 items)
   float* y;
   int groups, tiles, chunks;
   double inv_blocks, inv_chunks;  // 1 / grid size, 1 / chunks (exact floors of n b / P, n c / C)
 };
 
-// Everything the block keeps in LDS, carved from the dynamic allocation.
-template <int B>
+// Everything the block keeps in LDS (carved from the dynamic allocation),
+// sized for batches of up to BM tokens and rows of up to NU * 512 values.
+template <int BM, int NU>
 struct LayerLds {
+  static constexpr int kUnits = NU * kWave;   // 16-byte units of a token
+  static constexpr int kFold = kLWaves / BM;  // per-wave partial tiles held at once in the fold
   // tokens (fp16); once the gate/up work is done, the down-projection's
-  // per-wave tile sums: [8 wave pairs][B][512 columns]
+  // per-wave partial tiles
   union {
-    u32x4 xs[B * kMaxD / 8];
-    float dpart[8][B][kTile];
+    u32x4 xs[BM * kUnits];
+    float dpart[kFold][BM][kTile];
   };
-  uint32_t xw[B * kMaxD / 32];          // sign words of the tokens
-  int cpart[kLWaves][B][kWave];         // per-wave N_neg partial counts of the current group
-  uint32_t pm[4 * kMaxLayerGroups];     // published masks of every group
+  uint32_t xw[BM * kUnits / 4];  // sign words of the tokens
+  // per-wave N_neg partial counts during the prediction; the published masks
+  // of every group and their prefix afterwards
+  union {
+    int cpart[kLWaves][BM][kWave];
+    struct {
+      uint32_t pm[4 * kMaxLayerGroups];
+      int pre[kMaxLayerGroups];
+    } ex;
+  };
   int wtot[kLWaves];
-  int pre[kMaxLayerGroups];             // inclusive prefix of the kept counts
-  int gfirst[2];                        // group holding the first position of the slice / the down item
-  float dots[kRoundRows][2][B];         // W_gate . x and W_up . x of the round's rows
-  float h1[kRoundRows][B];
-  uint32_t need[kRoundRows];            // round row needs a late W_up read
-  uint32_t srow[kMaxSlice];             // conf << 31 | row of the block's gate/up positions
-  uint32_t dent[kMaxDownItem];          // conf << 31 | row of the block's down positions
-  float hs[kDownRound][B];              // h3 of the down round's positions
-  int sc[8];                            // block scalars: n, lo, hi, dlo, dhi
+  int gfirst[2];                  // group holding the first position of the slice / the down item
+  float dots[kRoundRows][2][BM];  // W_gate . x and W_up . x of the round's rows
+  float h1[kRoundRows][BM];
+  uint32_t need[kRoundRows];      // round row needs a late W_up read
+  uint32_t srow[kMaxSlice];       // conf << 31 | row of the block's gate/up positions
+  uint32_t dent[kMaxDownItem];    // conf << 31 | row of the block's down positions
+  float hs[kDownRound * BM];      // h3 of the down round's positions
+  int sc[8];                      // block scalars: lo, hi, dlo, dhi
   int n_late, n_up, n_down, zok;
   uint32_t epoch;
 };
+
+template <int BM, int NU>
+constexpr int layer_lds_bytes() {
+  const int need = (int)((sizeof(LayerLds<BM, NU>) + 1023) / 1024 * 1024);
+  return need < kMinLds ? kMinLds : need;
+}
 
 __device__ inline uint64_t tagged(uint32_t tag, uint32_t payload) { return ((uint64_t)tag << 32) | payload; }
 
@@ -190,67 +223,76 @@ __device__ inline uint32_t poll_lane(const uint64_t* p, bool active, uint32_t ta
   return out;
 }
 
-// Index of the n-th (0-based) set bit of m; m must have more than n bits set.
-__device__ inline int nth_set_bit(uint64_t m, int n) {
-  int pos = 0;
-#pragma unroll
-  for (int s = 32; s >= 1; s >>= 1) {
-    const uint64_t low = m & ((1ull << s) - 1ull);
-    const int c = __popcll(low);
-    if (n >= c) {
-      n -= c;
-      m >>= s;
-      pos += s;
-    } else {
-      m = low;
+// Threads [0, nthreads) wait until every block's alive word carries `tag`.
+__device__ inline void wait_alive(const uint64_t* alive, int blocks, int t, int nthreads, uint32_t tag,
+                                  uint32_t* hdr) {
+  for (int j = t; j < blocks; j += nthreads) {
+    long spins = 0;
+    while ((uint32_t)(ld_agent64(&alive[j]) >> 32) != tag) {
+      if (++spins > kPollLimit) {
+        atomicOr(&hdr[H_ERR], kErrLookbackSpin);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
     }
   }
-  return pos;
 }
 
+// Block 0, once every block has read the call counter: advance it.
+__device__ inline void advance_epoch(uint32_t* hdr, uint32_t epoch) { st_agent(&hdr[H_EPOCH], epoch + 1u); }
+
 // Dot products of a row held as NU 16-byte units per lane (unit lane + 64 j)
-// with the B tokens in LDS; wave-uniform results.
-template <int B, int NU>
-__device__ inline void row_dots(const u32x4 (&v)[NU], const u32x4* xs, int U, int lane, float (&out)[B]) {
-  float acc[B];
+// with the BM tokens in LDS; wave-uniform results.
+// Units past the row's end (u >= U) hold a repeat of its last unit and are
+// left out with a select, not a branch.
+template <int BM, int NU>
+__device__ inline void row_dots(const u32x4 (&v)[NU], const u32x4* xs, int U, int lane, float (&out)[BM]) {
+  float acc[BM];
 #pragma unroll
-  for (int t = 0; t < B; ++t) acc[t] = 0.f;
+  for (int t = 0; t < BM; ++t) acc[t] = 0.f;
 #pragma unroll
   for (int j = 0; j < NU; ++j) {
     const int u = lane + kWave * j;
-    if (u < U) {
+    const int uc = min(u, U - 1);
 #pragma unroll
-      for (int t = 0; t < B; ++t) acc[t] = dot8(v[j], xs[t * U + u], acc[t]);
+    for (int t = 0; t < BM; ++t) {
+      const float s = dot8(v[j], xs[t * U + uc], acc[t]);
+      acc[t] = u < U ? s : acc[t];
     }
   }
 #pragma unroll
-  for (int t = 0; t < B; ++t) out[t] = wave_total(acc[t]);
+  for (int t = 0; t < BM; ++t) out[t] = wave_total(acc[t]);
 }
 
+// All NU requests of a row in straight-line code (no per-unit branches, so
+// the compiler can count them and issue them back to back); units past the
+// row's end repeat its last unit.
 template <int NU>
 __device__ inline void load_row(const u32x4* __restrict__ row, int U, int lane, u32x4 (&v)[NU]) {
 #pragma unroll
-  for (int j = 0; j < NU; ++j) {
-    const int u = lane + kWave * j;
-    if (u < U) v[j] = load_nt(row + u);
-  }
+  for (int j = 0; j < NU; ++j) v[j] = load_nt(row + min(lane + kWave * j, U - 1));
 }
 
-template <int B, int NU>
+template <int BM, int NU>
 __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
-  LayerLds<B>& L = *reinterpret_cast<LayerLds<B>*>(lds_raw);
+  LayerLds<BM, NU>& L = *reinterpret_cast<LayerLds<BM, NU>*>(lds_raw);
 
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int d = a.d, U = d >> 3, W = d >> 5, units = d >> 7;
+  const int b = a.b;  // tokens, 1..BM; tokens b..BM-1 are zero
   const int P = gridDim.x, blk = blockIdx.x, G = a.groups;
   const int T = a.tiles;
+  const int mode = a.mode;
   const bool no_as = (a.flags & kNoAS) != 0;
   const bool spec_ok = (a.flags & kNoSpec) == 0;
 
   SI_TRACE_MARK(0);
-  // ---- tokens, then the sign loads of the block's first group
-  for (int i = tid; i < B * U; i += kLThreads) L.xs[i] = reinterpret_cast<const u32x4*>(a.x)[i];
+  // ---- the packed signs of the block's first group are requested, then
+  // the tokens and (behind the first token requests, so that the wait for
+  // it, which comes at once for an atomic load, also covers them) the call
+  // counter; addresses are clamped so that the requests are unconditional
+  // and go out back to back; tokens b..BM-1 are zero
   u32x4 sreg[kMaxSignUnitsPerWave];
   auto load_signs = [&](int g) {
     const u32x4* sg = a.signs + (size_t)g * units * kRowGroup + lane;
@@ -260,83 +302,110 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
       if (q < units) sreg[i] = load_nt(sg + (size_t)q * kRowGroup);
     }
   };
-  if (blk < G) load_signs(blk);
-  if (tid == 0) {
-    L.n_up = 0;
-    L.n_down = 0;
-    L.zok = 0;
-    L.epoch = ld_agent(&a.hdr[H_EPOCH]);
+  if (mode == kModePredict && blk < G) load_signs(blk);
+  {
+    const u32x4* xg = reinterpret_cast<const u32x4*>(a.x);
+    const int nx = b * U;
+    for (int i = tid; i < BM * U; i += kLThreads) {
+      const u32x4 xv = xg[min(i, nx - 1)];
+      if (i == tid && tid == 0) {
+        asm volatile("" ::: "memory");
+        L.epoch = ld_agent(&a.hdr[H_EPOCH]);
+        L.n_up = 0;
+        L.n_down = 0;
+        L.zok = 0;
+      }
+      L.xs[i] = i < nx ? xv : u32x4{0, 0, 0, 0};
+    }
   }
   __syncthreads();
   const uint32_t epoch = uniform(L.epoch);
   const uint32_t tag = epoch_tag(epoch);
-  for (int i = tid; i < B * W; i += kLThreads) {
-    const int t = i / W, w = i - t * W;
-    L.xw[i] = sign_word(&L.xs[t * U + 4 * w]);
+  if (tid == 0 && (mode == kModeList || blk >= G))  // this block has read the call counter
+    st_agent64(&a.alive[blk], tagged(tag, 0u));
+  if (mode == kModePredict) {
+    for (int i = tid; i < b * W; i += kLThreads) {
+      const int t = i / W, w = i - t * W;
+      L.xw[i] = sign_word(&L.xs[t * U + 4 * w]);
+    }
   }
   __syncthreads();
   SI_TRACE_MARK(1);
 
-  // ---- 1. predict the block's groups
-  for (int g = blk; g < G; g += P) {
-    if (g != blk) load_signs(g);
-    int c[B];
+  // ---- 1. the kept and confident rows of the block's groups
+  if (mode != kModeList) {
+    for (int g = blk; g < G; g += P) {
+      if (mode == kModePredict) {
+        if (g != blk) load_signs(g);
+        int c[BM];
 #pragma unroll
-    for (int t = 0; t < B; ++t) c[t] = 0;
-    bool any_unit = false;
+        for (int t = 0; t < BM; ++t) c[t] = 0;
+        bool any_unit = false;
 #pragma unroll
-    for (int i = 0; i < kMaxSignUnitsPerWave; ++i) {
-      const int q = wv + kLWaves * i;
-      if (q < units) {
-        any_unit = true;
+        for (int i = 0; i < kMaxSignUnitsPerWave; ++i) {
+          const int q = wv + kLWaves * i;
+          if (q < units) {
+            any_unit = true;
 #pragma unroll
-        for (int t = 0; t < B; ++t) {
-          const u32x4 xv = *reinterpret_cast<const u32x4*>(&L.xw[t * W + 4 * q]);
-          c[t] += __popc(sreg[i].x ^ xv.x) + __popc(sreg[i].y ^ xv.y) + __popc(sreg[i].z ^ xv.z) +
-                  __popc(sreg[i].w ^ xv.w);
+            for (int t = 0; t < BM; ++t) {
+              if (t < b) {
+                const u32x4 xv = *reinterpret_cast<const u32x4*>(&L.xw[t * W + 4 * q]);
+                c[t] += __popc(sreg[i].x ^ xv.x) + __popc(sreg[i].y ^ xv.y) + __popc(sreg[i].z ^ xv.z) +
+                        __popc(sreg[i].w ^ xv.w);
+              }
+            }
+          }
+        }
+        if (any_unit) {
+#pragma unroll
+          for (int t = 0; t < BM; ++t)
+            if (t < b) L.cpart[wv][t][lane] = c[t];
+        }
+        __syncthreads();
+      }
+      if (wv == 0) {
+        const int row = g * kRowGroup + lane;
+        bool keep = false, conf = false;
+        if (mode == kModePredict) {
+          const int nw = min(units, kLWaves);  // waves that counted units
+#pragma unroll
+          for (int t = 0; t < BM; ++t) {
+            if (t < b) {
+              int n_neg = 0;
+              for (int w = 0; w < nw; ++w) n_neg += L.cpart[w][t][lane];
+              keep |= n_neg < a.T;
+              conf |= n_neg < a.T - a.margin;
+            }
+          }
+          keep = keep && row < a.k;
+          if (row < a.k) a.mask[row] = keep ? 1 : 0;
+        } else {  // mask mode: every kept row is treated as confident
+          keep = row < a.k && a.mask_in[row] != 0;
+          conf = keep;
+        }
+        const uint64_t kb = __ballot(keep);
+        const uint64_t cb = __ballot(keep && conf);
+        if (lane < 4) {
+          const uint64_t m = lane < 2 ? kb : cb;
+          st_agent64(&a.pub[(size_t)g * 4 + lane], tagged(tag, (uint32_t)(m >> (32 * (lane & 1)))));
         }
       }
+      __syncthreads();
     }
-    if (any_unit) {
-#pragma unroll
-      for (int t = 0; t < B; ++t) L.cpart[wv][t][lane] = c[t];
-    }
-    __syncthreads();
-    if (wv == 0) {
-      const int row = g * kRowGroup + lane;
-      const int nw = min(units, kLWaves);  // waves that counted units
-      bool keep = false, conf = false;
-#pragma unroll
-      for (int t = 0; t < B; ++t) {
-        int n_neg = 0;
-        for (int w = 0; w < nw; ++w) n_neg += L.cpart[w][t][lane];
-        keep |= n_neg < a.T;
-        conf |= n_neg < a.T - a.margin;
-      }
-      keep = keep && row < a.k;
-      if (row < a.k) a.mask[row] = keep ? 1 : 0;
-      const uint64_t kb = __ballot(keep);
-      const uint64_t cb = __ballot(keep && conf);
-      if (lane < 4) {
-        const uint64_t m = lane < 2 ? kb : cb;
-        st_agent64(&a.pub[(size_t)g * 4 + lane], tagged(tag, (uint32_t)(m >> (32 * (lane & 1)))));
-      }
-    }
-    __syncthreads();
   }
-  if (blk >= G && tid == 0) st_agent64(&a.alive[blk], tagged(tag, 0u));
   // the tile of y this block owns is zeroed while the masks are exchanged
-  const bool owns_tile = blk < T;
+  const bool owns_tile = a.mlp && blk < T;
   if (owns_tile) {
-    for (int i = tid; i < B * kTile; i += kLThreads) {
+    for (int i = tid; i < b * kTile; i += kLThreads) {
       const int t = i / kTile, col = blk * kTile + (i - t * kTile);
       if (col < d) __hip_atomic_store(&a.y[(size_t)t * d + col], 0.f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
   SI_TRACE_MARK(2);
 
-  // ---- 2. every group's masks (and the word of every block without a group)
-  {
+  // ---- 2. every group's masks and the words of the blocks without a group;
+  // then block 0 knows every block has read the call counter and advances it
+  if (mode != kModeList) {
     const int NWp = 4 * G;
     const int NW = NWp + (P > G ? P - G : 0);
     uint64_t v[kMaxPollWords / kLThreads];
@@ -357,7 +426,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
       for (int i = 0; i < kMaxPollWords / kLThreads; ++i) {
         const int j = tid + kLThreads * i;
         if (((pending >> i) & 1u) && (uint32_t)(v[i] >> 32) == tag) {
-          if (j < NWp) L.pm[j] = (uint32_t)v[i];
+          if (j < NWp) L.ex.pm[j] = (uint32_t)v[i];
           pending &= ~(1u << i);
         }
       }
@@ -367,7 +436,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
 #pragma unroll
           for (int i = 0; i < kMaxPollWords / kLThreads; ++i) {
             const int j = tid + kLThreads * i;
-            if (((pending >> i) & 1u) && j < NWp) L.pm[j] = 0u;
+            if (((pending >> i) & 1u) && j < NWp) L.ex.pm[j] = 0u;
           }
           break;
         }
@@ -375,24 +444,53 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
       }
     }
   }
-  if (owns_tile) wait_own_stores();  // the y-zeroing stores of this wave have landed
+  // every load of this wave has been consumed by now; waiting here (at no
+  // cost) also tells the compiler so, and it then issues the gate/up row
+  // requests back to back (without waits between them); owners also know
+  // their y-zeroing stores have landed
+  wait_own_stores();
   __syncthreads();
   if (tid == 0) {
     if (owns_tile) st_agent64(&a.zflag[blk], tagged(tag, 1u));
-    if (blk == 0) st_agent(&a.hdr[H_EPOCH], epoch + 1u);  // every block has read the call counter
+    if (mode != kModeList && blk == 0) advance_epoch(a.hdr, epoch);
   }
   SI_TRACE_MARK(3);
 
-  // ---- plan: kept count of every group (one group per thread) and their
-  // block-wide prefix; the block's gate/up slice and down item; then one
-  // wave per group that holds positions of them writes their list entries
-  // (lane = row: rank among the group's kept rows)
+  // ---- 3. plan: the block's gate/up slice and down item, and the list
+  // entries that fall in them
   const int C = a.chunks;
-  const bool has_item = blk < T * C;
+  const bool has_item = a.mlp && blk < T * C;
   const int tile = has_item ? blk % T : 0, chunk = has_item ? blk / T : 0;
-  {
+  if (mode == kModeList) {
+    const int n = min(max(*a.n_in, 0), a.k);
+    const int lo_ = (int)(((double)n * blk + 0.5) * a.inv_blocks);
+    const int hi_ = (int)(((double)n * (blk + 1) + 0.5) * a.inv_blocks);
+    const int dlo_ = has_item ? (int)(((double)n * chunk + 0.5) * a.inv_chunks) : 0;
+    const int dhi_ = has_item ? (int)(((double)n * (chunk + 1) + 0.5) * a.inv_chunks) : 0;
+    const uint32_t cbit = (spec_ok || no_as) ? 0x80000000u : 0u;  // given rows count as confident
+    for (int q = tid; q < hi_ - lo_; q += kLThreads) {
+      const int r = a.idx_in[lo_ + q];
+      const bool ok = (unsigned)r < (unsigned)a.k;
+      if (!ok) atomicOr(&a.hdr[H_ERR], kErrRow);
+      L.srow[q] = ok ? ((uint32_t)r | cbit) : kBadRow;
+    }
+    for (int q = tid; q < dhi_ - dlo_; q += kLThreads) {
+      const int r = a.idx_in[dlo_ + q];
+      const bool ok = (unsigned)r < (unsigned)a.k;
+      L.dent[q] = ok ? ((uint32_t)r | cbit) : kBadRow;
+    }
+    if (tid == 0) {
+      L.sc[1] = lo_;
+      L.sc[2] = hi_;
+      L.sc[3] = dlo_;
+      L.sc[4] = dhi_;
+    }
+  } else {
+    // kept count of every group (one group per thread) and their block-wide
+    // prefix; then one wave per group that holds positions of the block's
+    // ranges writes their list entries (lane = row: rank among the kept rows)
     uint64_t km = 0;
-    if (tid < G) km = (uint64_t)L.pm[4 * tid] | ((uint64_t)L.pm[4 * tid + 1] << 32);
+    if (tid < G) km = (uint64_t)L.ex.pm[4 * tid] | ((uint64_t)L.ex.pm[4 * tid + 1] << 32);
     const int c = __popcll(km);
     const int incl = wave_incl_scan(c);
     if (lane == kWave - 1) L.wtot[wv] = incl;
@@ -408,7 +506,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
     const int dhi_ = has_item ? (int)(((double)n * (chunk + 1) + 0.5) * a.inv_chunks) : 0;
     const int pi = before + incl, pe = pi - c;  // the group's kept rows hold positions [pe, pi)
     if (tid < G) {
-      L.pre[tid] = pi;
+      L.ex.pre[tid] = pi;
       if (lo_ < hi_ && pe <= lo_ && lo_ < pi) L.gfirst[0] = tid;
       if (dlo_ < dhi_ && pe <= dlo_ && dlo_ < pi) L.gfirst[1] = tid;
     }
@@ -424,12 +522,12 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
     const bool down_side = wv >= kLWaves / 2;
     const int rlo = down_side ? dlo_ : lo_, rhi = down_side ? dhi_ : hi_;
     for (int g = uniform(L.gfirst[down_side ? 1 : 0]) + (wv & 7); g < G; g += kLWaves / 2) {
-      const int gpi = L.pre[g];
-      const uint64_t gk = (uint64_t)L.pm[4 * g] | ((uint64_t)L.pm[4 * g + 1] << 32);
+      const int gpi = L.ex.pre[g];
+      const uint64_t gk = (uint64_t)L.ex.pm[4 * g] | ((uint64_t)L.ex.pm[4 * g + 1] << 32);
       const int gpe = gpi - __popcll(gk);
       if (gpe >= rhi) break;
       if (gpi <= rlo) continue;
-      const uint64_t gc = (uint64_t)L.pm[4 * g + 2] | ((uint64_t)L.pm[4 * g + 3] << 32);
+      const uint64_t gc = (uint64_t)L.ex.pm[4 * g + 2] | ((uint64_t)L.ex.pm[4 * g + 3] << 32);
       const int q = gpe + __popcll(gk & lanes_below(lane));
       if (((gk >> lane) & 1ull) && q >= rlo && q < rhi) {
         const uint32_t e = (uint32_t)(g * kRowGroup + lane) | (((gc >> lane) & 1ull) ? 0x80000000u : 0u);
@@ -446,6 +544,13 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
   const int lo = uniform(L.sc[1]), hi = uniform(L.sc[2]);
   const int dlo = uniform(L.sc[3]), dhi = uniform(L.sc[4]);
   SI_TRACE_MARK(4);
+  if (!a.mlp) {  // the predictor alone
+    if (tid == 0) {
+      a.counts[2 * blk] = 0;
+      a.counts[2 * blk + 1] = 0;
+    }
+    return;
+  }
 
   // ---- down requests of a round: this wave's positions q0 + wv + 16 j
   u32x4 vd[kDN];
@@ -460,7 +565,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
       const int q = wv + kLWaves * j;
       if (q0 + q < dhi) {
         const uint32_t e = L.dent[q0 - dlo + q];
-        if ((spec_ok && (e >> 31)) || no_as) {
+        if (e != kBadRow && ((spec_ok && (e >> 31)) || no_as)) {
           if (dcol_ok) vd[j] = load_nt(a.wdt + (size_t)(e & 0x7fffffffu) * U + dunit);
           dloaded |= 1u << j;
         }
@@ -468,27 +573,26 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
     }
   };
 
-  // ---- 3. gate/up: per round, wave wv owns item (row wv / 2, W_gate or W_up)
+  // ---- 4. gate/up: per round, wave wv owns item (row wv / 2, W_gate or W_up)
   const int ir = wv >> 1, imat = wv & 1;
   bool first = true;
   for (int r0 = lo; r0 < hi; r0 += kRoundRows) {
     const int mr = min(kRoundRows, hi - r0);
     const uint32_t* srow = &L.srow[r0 - lo];
     if (!first) __syncthreads();
-    bool active = false;
-    u32x4 v[NU];
-    if (ir < mr) {
-      const uint32_t e = srow[ir];
-      active = imat == 0 || (spec_ok && (e >> 31));
-      if (active) load_row<NU>((imat ? a.wu : a.wg) + (size_t)(e & 0x7fffffffu) * U, U, lane, v);
-    }
-    SI_TRACE_WAVE(0);
-    if (active) {
-      float dt[B];
-      row_dots<B, NU>(v, L.xs, U, lane, dt);
+    const uint32_t e = ir < mr ? srow[ir] : kBadRow;
+    // the row's requests and their use sit in one branch, so that no request
+    // is left outstanding across rounds (the compiler then issues them back
+    // to back instead of waiting before each)
+    if (e != kBadRow && (imat == 0 || (spec_ok && (e >> 31)))) {
+      u32x4 v[NU];
+      load_row<NU>((imat ? a.wu : a.wg) + (size_t)(e & 0x7fffffffu) * U, U, lane, v);
+      SI_TRACE_WAVE(0);
+      float dt[BM];
+      row_dots<BM, NU>(v, L.xs, U, lane, dt);
       if (lane == 0) {
 #pragma unroll
-        for (int t = 0; t < B; ++t) L.dots[ir][imat][t] = dt[t];
+        for (int t = 0; t < BM; ++t) L.dots[ir][imat][t] = dt[t];
       }
     }
     SI_TRACE_WAVE(1);
@@ -498,15 +602,17 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
     first = false;
     __syncthreads();
     if (wv == 0) {  // rows of the round: one per lane (mr <= 8)
-      bool any = no_as, spec = false;
+      bool any = no_as, spec = false, ok = false;
       if (lane < mr) {
+        ok = srow[lane] != kBadRow;
 #pragma unroll
-        for (int t = 0; t < B; ++t) {
-          const float h = fmaxf(L.dots[lane][0][t], 0.f);
+        for (int t = 0; t < BM; ++t) {
+          const float h = ok ? fmaxf(L.dots[lane][0][t], 0.f) : 0.f;
           L.h1[lane][t] = h;
           any |= h > 0.f;
         }
-        spec = spec_ok && (srow[lane] >> 31);
+        any = any && ok;
+        spec = ok && spec_ok && (srow[lane] >> 31);
         L.need[lane] = (any && !spec) ? 1u : 0u;
       }
       const uint64_t late = __ballot(lane < mr && any && !spec);
@@ -519,95 +625,133 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
     __syncthreads();
     if (L.n_late) {  // W_up rows whose gate value asks for them
       if (imat == 1 && ir < mr && L.need[ir]) {
+        u32x4 v[NU];
         load_row<NU>(a.wu + (size_t)(srow[ir] & 0x7fffffffu) * U, U, lane, v);
-        float dt[B];
-        row_dots<B, NU>(v, L.xs, U, lane, dt);
+        float dt[BM];
+        row_dots<BM, NU>(v, L.xs, U, lane, dt);
         if (lane == 0) {
 #pragma unroll
-          for (int t = 0; t < B; ++t) L.dots[ir][1][t] = dt[t];
+          for (int t = 0; t < BM; ++t) L.dots[ir][1][t] = dt[t];
         }
       }
       __syncthreads();
     }
-    if (tid < mr * B) {
-      const int r = tid / B, t = tid - r * B;
-      const bool spec = spec_ok && (srow[r] >> 31);
+    for (int i = tid; i < mr * b; i += kLThreads) {
+      const int r = i / b, t = i - r * b;
+      const bool spec = srow[r] != kBadRow && spec_ok && (srow[r] >> 31);
       const float h = (L.need[r] || spec) ? L.h1[r][t] * L.dots[r][1][t] : 0.f;
-      st_agent64(&a.h3e[(size_t)(r0 + r) * B + t], tagged(tag, __float_as_uint(h)));
+      st_agent64(&a.h3e[(size_t)(r0 + r) * b + t], tagged(tag, __float_as_uint(h)));
     }
   }
   if (first && dlo < dhi) issue_down(dlo);  // blocks without gate/up rows
   SI_TRACE_MARK(6);
 
-  // ---- 4. down-projection of (tile, chunk)
-  float acc[B][8];
+  // ---- 5. down-projection of (tile, chunk)
+  float acc[BM][8];
 #pragma unroll
-  for (int t = 0; t < B; ++t)
+  for (int t = 0; t < BM; ++t)
 #pragma unroll
     for (int q = 0; q < 8; ++q) acc[t][q] = 0.f;
-  bool abort = false;
   int n_down = 0;
+  bool epoch_done = mode != kModeList;
   for (int q0 = dlo; q0 < dhi; q0 += kDownRound) {
     const int nq = min(kDownRound, dhi - q0);
     if (q0 != dlo) {
       __syncthreads();  // the previous round's h3 values have been used
       issue_down(q0);
     }
-    // wave 0 collects the round's h3 (contiguous words, one position per
-    // lane); in the first round wave 1 checks the tile's zero flag
-    if (wv == 0) {
+    // waves 0..3 collect the round's h3 words (contiguous: positions x
+    // tokens, all requests in flight together); in the first round wave 4
+    // checks the tile's zero flag and, in list mode, waves 8.. of block 0
+    // collect every block's alive word
+    if (tid < kDownPollThreads) {
+      constexpr int kPer = (kDownRound * BM + kDownPollThreads - 1) / kDownPollThreads;
+      const int nw = nq * b;
+      const uint64_t* base = &a.h3e[(size_t)q0 * b];
+      uint64_t w[kPer];
+      uint32_t pending = 0;
 #pragma unroll
-      for (int t = 0; t < B; ++t) {
-        const bool mine = lane < nq;
-        const float h = __uint_as_float(poll_lane(&a.h3e[(size_t)(q0 + (mine ? lane : 0)) * B + t], mine, tag,
-                                                  a.hdr, abort));
-        if (mine) L.hs[lane][t] = abort ? 0.f : h;
+      for (int i = 0; i < kPer; ++i)
+        if (tid + kDownPollThreads * i < nw) pending |= 1u << i;
+      long spins = 0;
+      while (pending) {
+#pragma unroll
+        for (int i = 0; i < kPer; ++i)
+          if ((pending >> i) & 1u) w[i] = ld_agent64(base + tid + kDownPollThreads * i);
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+          if (((pending >> i) & 1u) && (uint32_t)(w[i] >> 32) == tag) {
+            L.hs[tid + kDownPollThreads * i] = __uint_as_float((uint32_t)w[i]);
+            pending &= ~(1u << i);
+          }
+        }
+        if (pending) {
+          if (++spins > kPollLimit) {
+            atomicOr(&a.hdr[H_ERR], kErrLookbackSpin);
+#pragma unroll
+            for (int i = 0; i < kPer; ++i)
+              if ((pending >> i) & 1u) L.hs[tid + kDownPollThreads * i] = 0.f;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+        }
       }
-    } else if (wv == 1 && q0 == dlo) {
+    } else if (q0 == dlo && wv == kDownPollThreads / kWave) {
+      bool abort = false;
       poll_lane(&a.zflag[tile], lane == 0, tag, a.hdr, abort);
       if (lane == 0 && !abort) L.zok = 1;
+    } else if (q0 == dlo && !epoch_done && blk == 0 && wv >= kLWaves / 2) {
+      wait_alive(a.alive, P, tid - kLThreads / 2, kLThreads / 2, tag, a.hdr);
     }
     __syncthreads();
+    if (q0 == dlo && !epoch_done && blk == 0 && tid == 0) advance_epoch(a.hdr, epoch);
+    epoch_done = true;
     if (q0 == dlo) SI_TRACE_WAVE(3);
 #pragma unroll
     for (int j = 0; j < kDN; ++j) {
       const int q = wv + kLWaves * j;
-      float hv[B];
+      float hv[BM];
       bool nz = false;
 #pragma unroll
-      for (int t = 0; t < B; ++t) {
-        hv[t] = q < nq ? L.hs[q][t] : 0.f;
+      for (int t = 0; t < BM; ++t) {
+        hv[t] = (q < nq && t < b) ? L.hs[q * b + t] : 0.f;
         nz |= hv[t] != 0.f;
       }
       if (q < nq && !((dloaded >> j) & 1u) && nz) {  // late request
-        if (dcol_ok) vd[j] = load_nt(a.wdt + (size_t)(L.dent[q0 - dlo + q] & 0x7fffffffu) * U + dunit);
-        dloaded |= 1u << j;
+        const uint32_t e = L.dent[q0 - dlo + q];
+        if (e != kBadRow) {
+          if (dcol_ok) vd[j] = load_nt(a.wdt + (size_t)(e & 0x7fffffffu) * U + dunit);
+          dloaded |= 1u << j;
+        }
       }
       const f16x2 p0 = as_h2(vd[j].x), p1 = as_h2(vd[j].y), p2 = as_h2(vd[j].z), p3 = as_h2(vd[j].w);
       const float f[8] = {(float)p0.x, (float)p0.y, (float)p1.x, (float)p1.y,
                           (float)p2.x, (float)p2.y, (float)p3.x, (float)p3.y};
 #pragma unroll
-      for (int t = 0; t < B; ++t)
+      for (int t = 0; t < BM; ++t)
 #pragma unroll
         for (int qq = 0; qq < 8; ++qq) acc[t][qq] = fmaf(hv[t], f[qq], acc[t][qq]);
     }
     n_down += __popc(dloaded);
     if (q0 == dlo) SI_TRACE_WAVE(4);
   }
-  // per-wave tile sums folded in LDS (plain stores; x is no longer needed)
+  // per-wave partial tiles folded in LDS (plain stores; x is no longer
+  // needed): kFold waves store, the others add in turn
+  constexpr int kFold = LayerLds<BM, NU>::kFold;
   if (dlo < dhi) {
-    if (wv < 8) {
 #pragma unroll
-      for (int t = 0; t < B; ++t)
+    for (int pass = 0; pass < kLWaves / kFold; ++pass) {
+      if (wv / kFold == pass) {
+        const int s = wv - pass * kFold;
 #pragma unroll
-        for (int q = 0; q < 8; ++q) L.dpart[wv][t][lane * 8 + q] = acc[t][q];
-    }
-    __syncthreads();
-    if (wv >= 8) {
+        for (int t = 0; t < BM; ++t)
 #pragma unroll
-      for (int t = 0; t < B; ++t)
-#pragma unroll
-        for (int q = 0; q < 8; ++q) L.dpart[wv - 8][t][lane * 8 + q] += acc[t][q];
+          for (int q = 0; q < 8; ++q) {
+            float& dst = L.dpart[s][t][lane * 8 + q];
+            dst = pass == 0 ? acc[t][q] : dst + acc[t][q];
+          }
+      }
+      if (pass + 1 < kLWaves / kFold) __syncthreads();
     }
   }
   if (lane == 0 && tile == 0 && n_down) atomicAdd(&L.n_down, n_down);
@@ -628,13 +772,18 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
     }
     __syncthreads();
     SI_TRACE_MARK(9);
-    for (int i = tid; i < B * kTile; i += kLThreads) {
+    for (int i = tid; i < b * kTile; i += kLThreads) {
       const int t = i / kTile, c = i - t * kTile, col = tile * kTile + c;
       float v = 0.f;
 #pragma unroll
-      for (int w = 0; w < 8; ++w) v += L.dpart[w][t][c];
+      for (int s = 0; s < kFold; ++s) v += L.dpart[s][t][c];
       if (col < d && v != 0.f) unsafeAtomicAdd(&a.y[(size_t)t * d + col], v);
     }
+  }
+  if (!epoch_done && blk == 0) {  // list mode without a down round
+    wait_alive(a.alive, P, tid, kLThreads, tag, a.hdr);
+    __syncthreads();
+    if (tid == 0) advance_epoch(a.hdr, epoch);
   }
   SI_TRACE_MARK(10);
   if (tid == 0) {
@@ -676,112 +825,126 @@ inline int units_per_lane(int d) {
   return nu <= 1 ? 1 : nu <= 2 ? 2 : nu <= 4 ? 4 : nu <= 8 ? 8 : nu <= 10 ? 10 : 16;
 }
 
-// Grid of the single-kernel path: one block per compute unit (the LDS
-// request keeps a second block off every CU), or 0 if the kernel cannot be
-// resident on every CU.
-template <int B, int NU>
+// Batch bucket of the kernel: the smallest of 1, 2, 4, 8 that holds b.
+inline int batch_bucket(int b) { return b <= 1 ? 1 : b <= 2 ? 2 : b <= 4 ? 4 : 8; }
+
+// Grid of the single-kernel path: one block per compute unit, or 0 if the
+// kernel's LDS does not fit or it cannot be resident on every CU.
+template <int BM, int NU>
 static int layer_blocks() {
   static int blocks = -1;
   if (blocks < 0) {
     blocks = 0;
-    int dev = 0, cus = 0, per_cu = 0;
-    static_assert(sizeof(LayerLds<B>) <= (size_t)kLayerLdsBytes, "LDS budget");
-    const void* fn = reinterpret_cast<const void*>(&k_layer<B, NU>);
-    if (hipGetDevice(&dev) != hipSuccess) return 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, kLayerLdsBytes) != hipSuccess) return 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kLThreads, kLayerLdsBytes) != hipSuccess) return 0;
-    if (per_cu >= 1) blocks = cus < kMaxLayerBlocks ? cus : kMaxLayerBlocks;
+    constexpr int lds = layer_lds_bytes<BM, NU>();
+    if constexpr (lds <= kMaxLds) {
+      int dev = 0, cus = 0, per_cu = 0;
+      const void* fn = reinterpret_cast<const void*>(&k_layer<BM, NU>);
+      if (hipGetDevice(&dev) != hipSuccess) return 0;
+      if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+      if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kLThreads, lds) != hipSuccess) return 0;
+      if (per_cu >= 1) blocks = cus < kMaxLayerBlocks ? cus : kMaxLayerBlocks;
+    }
   }
   return blocks;
 }
 
-#define SI_LAYER_DISPATCH(B, CALL)          \
-  switch (units_per_lane(d)) {             \
-    case 1: return CALL(B, 1);             \
-    case 2: return CALL(B, 2);             \
-    case 4: return CALL(B, 4);             \
-    case 8: return CALL(B, 8);             \
-    case 10: return CALL(B, 10);           \
-    default: return CALL(B, 16);           \
+template <int BM, int NU>
+static hipError_t layer_b(const LayerCall& c, hipStream_t s) {
+  if constexpr (layer_lds_bytes<BM, NU>() > kMaxLds) {
+    return hipErrorInvalidConfiguration;
+  } else {
+    const int k = c.k, d = c.d;
+    const WsLayout L = ws_layout(k, c.b);
+    char* base = static_cast<char*>(c.ws);
+    const int P = layer_blocks<BM, NU>();
+    if (P < 1) return hipErrorInvalidConfiguration;
+    LayerArgs a;
+    a.signs = reinterpret_cast<const u32x4*>(c.signs);
+    a.wg = reinterpret_cast<const u32x4*>(c.w_gate);
+    a.wu = reinterpret_cast<const u32x4*>(c.w_up);
+    a.wdt = reinterpret_cast<const u32x4*>(c.w_down_t);
+    a.x = c.x;
+    a.mask_in = c.mask_in;
+    a.idx_in = c.idx_in;
+    a.n_in = c.n_in;
+    a.k = k;
+    a.d = d;
+    a.b = c.b;
+    a.T = c.T;
+    a.margin = c.margin;
+    a.flags = c.flags;
+    a.mode = c.idx_in ? kModeList : c.mask_in ? kModeMask : kModePredict;
+    a.mlp = c.y != nullptr;
+    a.mask = c.mask;
+    a.idx = c.idx;
+    a.n_out = c.n_out;
+    a.hdr = reinterpret_cast<uint32_t*>(base);
+    a.pub = reinterpret_cast<uint64_t*>(base + L.lmask);
+    a.zflag = reinterpret_cast<uint64_t*>(base + L.zflag);
+    a.alive = reinterpret_cast<uint64_t*>(base + L.alive);
+    a.h3e = reinterpret_cast<uint64_t*>(base + L.h3e);
+    a.counts = reinterpret_cast<int32_t*>(base + L.counts);
+    a.y = c.y;
+    a.groups = row_groups(k);
+    a.tiles = (d + kTile - 1) / kTile;
+    a.chunks = P / a.tiles;
+    a.inv_blocks = 1.0 / P;
+    a.inv_chunks = 1.0 / a.chunks;
+    k_layer<BM, NU><<<P, kLThreads, layer_lds_bytes<BM, NU>(), s>>>(a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !c.counters || !c.y) return e;
+    k_sum_counts<<<1, 256, 0, s>>>(a.counts, P, c.idx_in ? c.n_in : c.n_out, k, c.counters);
+    return hipGetLastError();
+  }
+}
+
+#define SI_NU_DISPATCH(BM, CALL)   \
+  switch (units_per_lane(d)) {     \
+    case 1: return CALL(BM, 1);    \
+    case 2: return CALL(BM, 2);    \
+    case 4: return CALL(BM, 4);    \
+    case 8: return CALL(BM, 8);    \
+    case 10: return CALL(BM, 10);  \
+    default: return CALL(BM, 16);  \
+  }
+
+#define SI_LAYER_DISPATCH(CALL)        \
+  switch (batch_bucket(b)) {           \
+    case 1: SI_NU_DISPATCH(1, CALL)    \
+    case 2: SI_NU_DISPATCH(2, CALL)    \
+    case 4: SI_NU_DISPATCH(4, CALL)    \
+    default: SI_NU_DISPATCH(8, CALL)   \
   }
 
 static int blocks_for(int d, int b) {
-#define BLOCKS(B, NU) layer_blocks<B, NU>()
-  if (b == 1) { SI_LAYER_DISPATCH(1, BLOCKS) }
-  if (b == 2) { SI_LAYER_DISPATCH(2, BLOCKS) }
-  return 0;
+  if (b < 1 || b > kMaxB) return 0;
+#define BLOCKS(BM, NU) layer_blocks<BM, NU>()
+  SI_LAYER_DISPATCH(BLOCKS)
 #undef BLOCKS
 }
 
-// The single-kernel path applies for batches of at most two tokens, up to
-// kMaxLayerGroups row groups (every group's masks fit in LDS and in one
-// poll per thread), and when one block per CU can be resident.
+// The single-kernel path applies up to kMaxLayerGroups row groups (every
+// group's masks fit in LDS and in one poll per thread) and when one block per
+// CU can be resident with the LDS that the batch and row width need.
 bool layer_supported(int k, int d, int b) {
-  if (b < 1 || b > kLayerMaxB) return false;
   const int G = row_groups(k);
   if (G > kMaxLayerGroups) return false;
   const int P = blocks_for(d, b);
   const int tiles = (d + kTile - 1) / kTile;
   if (P < tiles) return false;
   const int chunks = P / tiles;
-  if ((k + P - 1) / P > kMaxSlice || (k + chunks - 1) / chunks > kMaxDownItem) return false;
-  return 4 * G + (P > G ? P - G : 0) <= kMaxPollWords;
+  if (4 * G + (P > G ? P - G : 0) > kMaxPollWords) return false;
+  return (k + P - 1) / P <= kMaxSlice && (k + chunks - 1) / chunks <= kMaxDownItem;
 }
 
-template <int B, int NU>
-static hipError_t layer_b(const uint32_t* signs, const uint16_t* w_gate, const uint16_t* w_up,
-                          const uint16_t* w_down_t, int k, int d, const uint16_t* x, int T, int margin,
-                          uint8_t* mask, int32_t* idx, int32_t* n_out, float* y, void* ws, uint32_t flags,
-                          int32_t* counters, hipStream_t s) {
-  const WsLayout L = ws_layout(k, B);
-  char* base = static_cast<char*>(ws);
-  const int P = layer_blocks<B, NU>();
-  if (P < 1) return hipErrorInvalidConfiguration;
-  LayerArgs a;
-  a.signs = reinterpret_cast<const u32x4*>(signs);
-  a.wg = reinterpret_cast<const u32x4*>(w_gate);
-  a.wu = reinterpret_cast<const u32x4*>(w_up);
-  a.wdt = reinterpret_cast<const u32x4*>(w_down_t);
-  a.x = x;
-  a.k = k;
-  a.d = d;
-  a.T = T;
-  a.margin = margin;
-  a.flags = flags;
-  a.mask = mask;
-  a.idx = idx;
-  a.n_out = n_out;
-  a.hdr = reinterpret_cast<uint32_t*>(base);
-  a.pub = reinterpret_cast<uint64_t*>(base + L.lmask);
-  a.alive = reinterpret_cast<uint64_t*>(base + L.alive);
-  a.zflag = reinterpret_cast<uint64_t*>(base + L.zflag);
-  a.h3e = reinterpret_cast<uint64_t*>(base + L.h3e);
-  a.counts = reinterpret_cast<int32_t*>(base + L.counts);
-  a.y = y;
-  a.groups = row_groups(k);
-  a.tiles = (d + kTile - 1) / kTile;
-  a.chunks = P / a.tiles;
-  a.inv_blocks = 1.0 / P;
-  a.inv_chunks = 1.0 / a.chunks;
-  k_layer<B, NU><<<P, kLThreads, kLayerLdsBytes, s>>>(a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !counters) return e;
-  k_sum_counts<<<1, 256, 0, s>>>(a.counts, P, n_out, k, counters);
-  return hipGetLastError();
-}
-
-hipError_t launch_layer(const uint32_t* signs, const uint16_t* w_gate, const uint16_t* w_up,
-                        const uint16_t* w_down_t, int k, int d, const uint16_t* x, int b, int T, int margin,
-                        uint8_t* mask, int32_t* idx, int32_t* n_out, float* y, void* ws, uint32_t flags,
-                        int32_t* counters, hipStream_t s) {
-#define LAUNCH(B, NU) \
-  layer_b<B, NU>(signs, w_gate, w_up, w_down_t, k, d, x, T, margin, mask, idx, n_out, y, ws, flags, counters, s)
-  if (b == 1) { SI_LAYER_DISPATCH(1, LAUNCH) }
-  if (b == 2) { SI_LAYER_DISPATCH(2, LAUNCH) }
-  return hipErrorInvalidValue;
+hipError_t launch_layer(const LayerCall& c, hipStream_t s) {
+  const int d = c.d, b = c.b;
+#define LAUNCH(BM, NU) layer_b<BM, NU>(c, s)
+  SI_LAYER_DISPATCH(LAUNCH)
 #undef LAUNCH
 }
 #undef SI_LAYER_DISPATCH
+#undef SI_NU_DISPATCH
 
 }  // namespace si

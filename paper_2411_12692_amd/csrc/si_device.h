@@ -40,7 +40,7 @@ struct WsLayout {
   size_t upflag;  // uint8 [k] 1 where the W_up row was read
   size_t lmask;   // uint64 [groups][4] single-kernel kept / confident masks
   size_t zflag;   // uint64 [64] single-kernel "tile of y zeroed" flags
-  size_t alive;   // uint64 [kMaxLayerBlocks] single-kernel words of blocks that own no row group
+  size_t alive;   // uint64 [kMaxLayerBlocks] single-kernel "this block has read the call counter" words
   size_t h3;      // float [k][b] h3 per row (valid on kept rows)
   size_t h3e;     // uint64 [groups][64][b] single-kernel h3 exchange words
   size_t total;

@@ -27,13 +27,32 @@ hipError_t launch_predict_gate_up(const uint32_t* signs, const uint16_t* w_gate,
 hipError_t launch_down(const uint16_t* w_down_t, int k, int d, int b, const int32_t* idx, const int32_t* n_active,
                        float* y, void* ws, int slots, uint32_t flags, int32_t* counters, hipStream_t s);
 
-// The whole path of one layer in one kernel (layer.hip).  Only valid when
-// layer_supported(k, d, b); `margin` gates the speculative row requests.
+// The path of one layer in one kernel (layer.hip).  The kept rows come from
+// the packed signs (predict: signs set, mask_in and idx_in NULL), from a
+// caller's mask (mask_in set) or from a caller's list (idx_in and n_in set);
+// y NULL runs the predictor alone.  Only valid when layer_supported(k, d, b).
+struct LayerCall {
+  const uint32_t* signs = nullptr;
+  const uint16_t* w_gate = nullptr;
+  const uint16_t* w_up = nullptr;
+  const uint16_t* w_down_t = nullptr;
+  const uint16_t* x = nullptr;
+  const uint8_t* mask_in = nullptr;
+  const int32_t* idx_in = nullptr;
+  const int32_t* n_in = nullptr;
+  int k = 0, d = 0, b = 1;
+  int T = 0;       // integer threshold of Eq. (2) (predict)
+  int margin = 0;  // rows with N_neg < T - margin are treated as surely kept (speculative requests)
+  uint32_t flags = 0;
+  uint8_t* mask = nullptr;   // predict: the mask
+  int32_t* idx = nullptr;    // predict and mask: the kept list
+  int32_t* n_out = nullptr;  // predict and mask: its length
+  float* y = nullptr;
+  void* ws = nullptr;
+  int32_t* counters = nullptr;
+};
 bool layer_supported(int k, int d, int b);
-hipError_t launch_layer(const uint32_t* signs, const uint16_t* w_gate, const uint16_t* w_up,
-                        const uint16_t* w_down_t, int k, int d, const uint16_t* x, int b, int T, int margin,
-                        uint8_t* mask, int32_t* idx, int32_t* n_out, float* y, void* ws, uint32_t flags,
-                        int32_t* counters, hipStream_t s);
+hipError_t launch_layer(const LayerCall& c, hipStream_t s);
 
 // mask -> ascending kept list and count (single block).
 hipError_t launch_compact(const uint8_t* mask, int k, int32_t* idx, int32_t* n_out, hipStream_t s);

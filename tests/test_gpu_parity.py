@@ -328,11 +328,13 @@ def test_13b_layer():
 
 @pytest.mark.parametrize("k,d,b,one", [(11008, 4096, 1, 1), (13824, 5120, 1, 1), (1376, 512, 1, 1),
                                        (11008, 4096, 2, 1), (1, 128, 1, 1), (61440, 128, 1, 1),
-                                       (61441, 128, 1, 0), (11008, 4096, 3, 0), (11008, 4096, 9, 0)])
+                                       (11008, 4096, 3, 1), (11008, 4096, 8, 1), (13824, 5120, 8, 1),
+                                       (129, 8192, 4, 1), (129, 8192, 5, 0), (61441, 128, 1, 0),
+                                       (11008, 4096, 9, 0)])
 def test_single_launch_path(k, d, b, one):
-    """The shapes the parity tests use at b <= 2 run the one-launch kernel
-    (so its results are the ones checked); larger batches and k take the
-    two-launch path."""
+    """The shapes the parity tests use run the one-launch kernel (so its
+    results are the ones checked); k above 61440 and batches of more than 4
+    tokens at d > 5120 take the two-launch path."""
     assert si._lib.load().si_single_launch(k, d, b) == one
 
 
