@@ -88,7 +88,7 @@ size_t si_workspace_bytes(int k, int d, int b) {
 
 int si_single_launch(int k, int d, int b) {
   if (check_kd(k, d) != SI_OK || check_b(b) != SI_OK) return 0;
-  return si::layer_supported(k, d, b) ? 1 : 0;
+  return si::layer_supported(k, d, b) && si::owned_supported(k, d, b) ? 1 : 0;
 }
 
 int32_t si_alpha_threshold(float alpha, int d) {
@@ -145,9 +145,7 @@ si_status si_predict(const uint32_t* signs, int k, int d, const uint16_t* x, int
   if (std::isnan(alpha) || alpha < 0.0f) return fail(SI_ERR_ALPHA, "alpha=%g must be >= 0 (or +inf)", (double)alpha);
   if (si_status s = check_ws(workspace, workspace_bytes, k, b)) return s;
   const int T = si_alpha_threshold(alpha, d);
-  if (si::layer_supported(k, d, b)) {
-    const si::WsLayout L = si::ws_layout(k, b);
-    char* base = static_cast<char*>(workspace);
+  if (si::owned_supported(k, d, b)) {
     si::LayerCall c;
     c.signs = signs;
     c.x = x;
@@ -156,10 +154,10 @@ si_status si_predict(const uint32_t* signs, int k, int d, const uint16_t* x, int
     c.b = b;
     c.T = T;
     c.mask = mask;
-    c.idx = active_idx ? active_idx : reinterpret_cast<int32_t*>(base + L.idx);
-    c.n_out = n_active ? n_active : reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;
+    c.idx = active_idx;
+    c.n_out = n_active;
     c.ws = workspace;
-    return hip_status(si::launch_layer(c, (hipStream_t)stream), "predict launch");
+    return hip_status(si::launch_owned(c, (hipStream_t)stream), "predict launch");
   }
   return hip_status(si::launch_predict(signs, k, d, x, b, T, mask, active_idx, n_active, workspace,
                                        (hipStream_t)stream),
@@ -194,7 +192,7 @@ si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint
   hipStream_t st = (hipStream_t)stream;
   const si::WsLayout L = si::ws_layout(k, b);
   char* base = static_cast<char*>(workspace);
-  if (si::layer_supported(k, d, b)) {
+  if (active_idx ? si::layer_supported(k, d, b) : si::owned_supported(k, d, b)) {
     si::LayerCall c;
     c.w_gate = w_gate;
     c.w_up = w_up;
@@ -204,18 +202,17 @@ si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint
     c.d = d;
     c.b = b;
     c.flags = flags;
-    if (active_idx) {
-      c.idx_in = active_idx;
-      c.n_in = n_active;
-    } else {
-      c.mask_in = mask;
-      c.idx = reinterpret_cast<int32_t*>(base + L.idx);
-      c.n_out = reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;
-    }
     c.y = y;
     c.ws = workspace;
     c.counters = counters;
-    return hip_status(si::launch_layer(c, st), "sparse_mlp launch");
+    if (active_idx) {
+      c.idx_in = active_idx;
+      c.n_in = n_active;
+      return hip_status(si::launch_layer(c, st), "sparse_mlp launch");
+    }
+    c.mask_in = mask;
+    c.n_out = reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;  // n_gate of the counters
+    return hip_status(si::launch_owned(c, st), "sparse_mlp launch");
   }
   if (!active_idx) {
     int32_t* idx = reinterpret_cast<int32_t*>(base + L.idx);
@@ -256,12 +253,10 @@ si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, c
   if (si_status s = check_ws(workspace, workspace_bytes, k, b)) return s;
   const si::WsLayout L = si::ws_layout(k, b);
   char* base = static_cast<char*>(workspace);
-  if (!mask) mask = reinterpret_cast<uint8_t*>(base + L.mask);
-  if (!active_idx) active_idx = reinterpret_cast<int32_t*>(base + L.idx);
   if (!n_active) n_active = reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;
   hipStream_t st = (hipStream_t)stream;
   const int T = si_alpha_threshold(alpha, d);
-  if (si::layer_supported(k, d, b)) {
+  if (si::owned_supported(k, d, b)) {
     si::LayerCall c;
     c.signs = signs;
     c.w_gate = w_gate;
@@ -280,8 +275,10 @@ si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, c
     c.y = y;
     c.ws = workspace;
     c.counters = counters;
-    return hip_status(si::launch_layer(c, st), "layer launch");
+    return hip_status(si::launch_owned(c, st), "layer launch");
   }
+  if (!mask) mask = reinterpret_cast<uint8_t*>(base + L.mask);
+  if (!active_idx) active_idx = reinterpret_cast<int32_t*>(base + L.idx);
   if (si_status s = hip_status(si::launch_predict_gate_up(signs, w_gate, w_up, k, d, x, b, T, mask, active_idx,
                                                           n_active, y, workspace, flags, st),
                                "predict/gate-up launch"))

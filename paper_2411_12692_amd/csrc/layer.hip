@@ -53,8 +53,7 @@
 // it.  Every wait is bounded: past a spin limit the block sets an error bit
 // in the workspace header and goes on without the data.
 
-#include "si_device.h"
-#include "si_launch.h"
+#include "layer_common.h"
 
 namespace si {
 
@@ -69,24 +68,9 @@ extern "C" hipError_t si_trace_wave_read(void* dst, size_t bytes) {
 }
 #endif
 
-constexpr int kLWaves = 16;
-constexpr int kLThreads = kLWaves * kWave;
-constexpr int kMaxSignUnitsPerWave = (kMaxD / 128 + kLWaves - 1) / kLWaves;  // 4
 constexpr int kMaxLayerGroups = 960;       // masks of every group are held in LDS (k <= 61440)
 constexpr int kMaxPollWords = 4 * kLThreads;
-constexpr int kRoundRows = kLWaves / 2;    // gate/up rows per round: one (row, matrix) item per wave
-constexpr int kDN = 4;                     // down pieces in flight per wave
-constexpr int kDownRound = kLWaves * kDN;  // down positions per round
 constexpr int kMaxSlice = 256;             // gate/up positions of one block (at most)
-constexpr int kMaxDownItem = 4096;         // positions of one down item (at most)
-constexpr int kDownPollThreads = 256;      // waves 0..3 collect a round's h3 words
-constexpr int kMinLds = 96 * 1024;         // more than half of a CU's LDS: one block per CU
-constexpr int kMaxLds = 160 * 1024;
-constexpr long kPollLimit = 1l << 16;
-constexpr uint32_t kNoAS = 1u, kNoSpec = 2u;
-constexpr uint32_t kBadRow = 0xffffffffu;  // list entry outside [0, k)
-static_assert(kTile == kWave * 8, "a down tile is one 16-byte unit per lane");
-
 enum : int { kModePredict = 0, kModeMask = 1, kModeList = 2 };
 
 struct LayerArgs {
@@ -156,123 +140,6 @@ constexpr int layer_lds_bytes() {
   return need < kMinLds ? kMinLds : need;
 }
 
-__device__ inline uint64_t tagged(uint32_t tag, uint32_t payload) { return ((uint64_t)tag << 32) | payload; }
-
-template <int CTRL>
-__device__ inline float dpp_add(float v) {
-  return v + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, true));
-}
-
-// Sum over the 64 lanes (wave-uniform result): DPP sums inside each row of 16
-// lanes, then the four row sums.
-__device__ inline float wave_total(float v) {
-  v = dpp_add<0xB1>(v);   // quad_perm(1,0,3,2)
-  v = dpp_add<0x4E>(v);   // quad_perm(2,3,0,1)
-  v = dpp_add<0x141>(v);  // row_half_mirror
-  v = dpp_add<0x140>(v);  // row_mirror
-  const int iv = __builtin_bit_cast(int, v);
-  return (__builtin_bit_cast(float, __builtin_amdgcn_readlane(iv, 0)) +
-          __builtin_bit_cast(float, __builtin_amdgcn_readlane(iv, 16))) +
-         (__builtin_bit_cast(float, __builtin_amdgcn_readlane(iv, 32)) +
-          __builtin_bit_cast(float, __builtin_amdgcn_readlane(iv, 48)));
-}
-
-__device__ inline int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
-
-template <int CTRL, int ROWS>
-__device__ inline int dpp_get(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xF, true);
-}
-
-// Inclusive prefix sum over the 64 lanes: shifts by 1, 2, 4, 8 inside each
-// row of 16 lanes, then the last lane of rows 0 and 1 broadcast forward.
-__device__ inline int wave_incl_scan(int v) {
-  v += dpp_get<0x111, 0xF>(v);  // row_shr:1
-  v += dpp_get<0x112, 0xF>(v);  // row_shr:2
-  v += dpp_get<0x114, 0xF>(v);  // row_shr:4
-  v += dpp_get<0x118, 0xF>(v);  // row_shr:8
-  v += dpp_get<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
-  v += dpp_get<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
-  return v;
-}
-
-// Poll one tagged word per lane (lanes may use different addresses) until it
-// carries `tag`; returns the payload.  After the spin limit the wave stops
-// waiting (`abort`) and the error bit is set.
-__device__ inline uint32_t poll_lane(const uint64_t* p, bool active, uint32_t tag, uint32_t* hdr, bool& abort) {
-  uint32_t out = 0;
-  bool pending = active;
-  long spins = 0;
-  while (__ballot(pending) && !abort) {
-    if (pending) {
-      const uint64_t v = ld_agent64(p);
-      if ((uint32_t)(v >> 32) == tag) {
-        out = (uint32_t)v;
-        pending = false;
-      }
-    }
-    if (__ballot(pending)) {
-      if (++spins > kPollLimit) {
-        abort = true;
-        if (pending) atomicOr(&hdr[H_ERR], kErrLookbackSpin);
-      } else {
-        __builtin_amdgcn_s_sleep(1);
-      }
-    }
-  }
-  return out;
-}
-
-// Threads [0, nthreads) wait until every block's alive word carries `tag`.
-__device__ inline void wait_alive(const uint64_t* alive, int blocks, int t, int nthreads, uint32_t tag,
-                                  uint32_t* hdr) {
-  for (int j = t; j < blocks; j += nthreads) {
-    long spins = 0;
-    while ((uint32_t)(ld_agent64(&alive[j]) >> 32) != tag) {
-      if (++spins > kPollLimit) {
-        atomicOr(&hdr[H_ERR], kErrLookbackSpin);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
-}
-
-// Block 0, once every block has read the call counter: advance it.
-__device__ inline void advance_epoch(uint32_t* hdr, uint32_t epoch) { st_agent(&hdr[H_EPOCH], epoch + 1u); }
-
-// Dot products of a row held as NU 16-byte units per lane (unit lane + 64 j)
-// with the BM tokens in LDS; wave-uniform results.
-// Units past the row's end (u >= U) hold a repeat of its last unit and are
-// left out with a select, not a branch.
-template <int BM, int NU>
-__device__ inline void row_dots(const u32x4 (&v)[NU], const u32x4* xs, int U, int lane, float (&out)[BM]) {
-  float acc[BM];
-#pragma unroll
-  for (int t = 0; t < BM; ++t) acc[t] = 0.f;
-#pragma unroll
-  for (int j = 0; j < NU; ++j) {
-    const int u = lane + kWave * j;
-    const int uc = min(u, U - 1);
-#pragma unroll
-    for (int t = 0; t < BM; ++t) {
-      const float s = dot8(v[j], xs[t * U + uc], acc[t]);
-      acc[t] = u < U ? s : acc[t];
-    }
-  }
-#pragma unroll
-  for (int t = 0; t < BM; ++t) out[t] = wave_total(acc[t]);
-}
-
-// All NU requests of a row in straight-line code (no per-unit branches, so
-// the compiler can count them and issue them back to back); units past the
-// row's end repeat its last unit.
-template <int NU>
-__device__ inline void load_row(const u32x4* __restrict__ row, int U, int lane, u32x4 (&v)[NU]) {
-#pragma unroll
-  for (int j = 0; j < NU; ++j) v[j] = load_nt(row + min(lane + kWave * j, U - 1));
-}
-
 template <int BM, int NU>
 __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
@@ -287,6 +154,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
   const bool no_as = (a.flags & kNoAS) != 0;
   const bool spec_ok = (a.flags & kNoSpec) == 0;
 
+  SI_TRACE_DECL;
   SI_TRACE_MARK(0);
   // ---- the packed signs of the block's first group are requested, then
   // the tokens and (behind the first token requests, so that the wait for
@@ -549,6 +417,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
       a.counts[2 * blk] = 0;
       a.counts[2 * blk + 1] = 0;
     }
+    SI_TRACE_FLUSH;
     return;
   }
 
@@ -786,6 +655,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
     if (tid == 0) advance_epoch(a.hdr, epoch);
   }
   SI_TRACE_MARK(10);
+  SI_TRACE_FLUSH;
   if (tid == 0) {
     a.counts[2 * blk] = L.n_up;
     a.counts[2 * blk + 1] = L.n_down;
@@ -818,15 +688,12 @@ __global__ __launch_bounds__(256) void k_sum_counts(const int32_t* __restrict__ 
     counters[2] = s[1];
   }
 }
-
-// 16-byte units per lane that cover a row of d fp16 values (template bucket).
-inline int units_per_lane(int d) {
-  const int nu = (d / 8 + kWave - 1) / kWave;
-  return nu <= 1 ? 1 : nu <= 2 ? 2 : nu <= 4 ? 4 : nu <= 8 ? 8 : nu <= 10 ? 10 : 16;
+hipError_t launch_sum_counts(const int32_t* counts, int slots, const int32_t* n_active, int k, int32_t* counters,
+                             hipStream_t s) {
+  k_sum_counts<<<1, 256, 0, s>>>(counts, slots, n_active, k, counters);
+  return hipGetLastError();
 }
 
-// Batch bucket of the kernel: the smallest of 1, 2, 4, 8 that holds b.
-inline int batch_bucket(int b) { return b <= 1 ? 1 : b <= 2 ? 2 : b <= 4 ? 4 : 8; }
 
 // Grid of the single-kernel path: one block per compute unit, or 0 if the
 // kernel's LDS does not fit or it cannot be resident on every CU.
@@ -894,28 +761,9 @@ static hipError_t layer_b(const LayerCall& c, hipStream_t s) {
     k_layer<BM, NU><<<P, kLThreads, layer_lds_bytes<BM, NU>(), s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !c.counters || !c.y) return e;
-    k_sum_counts<<<1, 256, 0, s>>>(a.counts, P, c.idx_in ? c.n_in : c.n_out, k, c.counters);
-    return hipGetLastError();
+    return launch_sum_counts(a.counts, P, c.idx_in ? c.n_in : c.n_out, k, c.counters, s);
   }
 }
-
-#define SI_NU_DISPATCH(BM, CALL)   \
-  switch (units_per_lane(d)) {     \
-    case 1: return CALL(BM, 1);    \
-    case 2: return CALL(BM, 2);    \
-    case 4: return CALL(BM, 4);    \
-    case 8: return CALL(BM, 8);    \
-    case 10: return CALL(BM, 10);  \
-    default: return CALL(BM, 16);  \
-  }
-
-#define SI_LAYER_DISPATCH(CALL)        \
-  switch (batch_bucket(b)) {           \
-    case 1: SI_NU_DISPATCH(1, CALL)    \
-    case 2: SI_NU_DISPATCH(2, CALL)    \
-    case 4: SI_NU_DISPATCH(4, CALL)    \
-    default: SI_NU_DISPATCH(8, CALL)   \
-  }
 
 static int blocks_for(int d, int b) {
   if (b < 1 || b > kMaxB) return 0;

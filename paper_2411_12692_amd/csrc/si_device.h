@@ -28,6 +28,7 @@ constexpr uint32_t kErrRow = 4u;           // kept-row index outside [0, k)
 
 constexpr int kGateUpMaxBlocks = 2048;     // grid cap of the list-driven gate/up kernel
 constexpr int kMaxLayerBlocks = 1024;      // grid cap of the single-kernel path
+constexpr int kOwnPubStride = 32;          // published words per block of the row-owning kernel
 
 // Workspace layout (byte offsets), identical on host and device.  Regions
 // whose size depends on the batch come last, so every other offset is the
@@ -41,6 +42,7 @@ struct WsLayout {
   size_t lmask;   // uint64 [groups][4] single-kernel kept / confident masks
   size_t zflag;   // uint64 [64] single-kernel "tile of y zeroed" flags
   size_t alive;   // uint64 [kMaxLayerBlocks] single-kernel "this block has read the call counter" words
+  size_t opub;    // uint64 [kMaxLayerBlocks][kOwnPubStride] row-owning kernel: masks and count per block
   size_t h3;      // float [k][b] h3 per row (valid on kept rows)
   size_t h3e;     // uint64 [groups][64][b] single-kernel h3 exchange words
   size_t total;
@@ -66,7 +68,8 @@ __host__ __device__ inline WsLayout ws_layout(int k, int b) {
   L.lmask = L.upflag + align256((size_t)k);
   L.zflag = L.lmask + align256(groups * 4 * sizeof(uint64_t));
   L.alive = L.zflag + align256(64 * sizeof(uint64_t));
-  L.h3 = L.alive + align256(kMaxLayerBlocks * sizeof(uint64_t));
+  L.opub = L.alive + align256(kMaxLayerBlocks * sizeof(uint64_t));
+  L.h3 = L.opub + align256((size_t)kMaxLayerBlocks * kOwnPubStride * sizeof(uint64_t));
   L.h3e = L.h3 + align256((size_t)k * b * sizeof(float));
   L.total = L.h3e + align256(groups * kRowGroup * (size_t)b * sizeof(uint64_t));
   return L;
@@ -201,31 +204,44 @@ __device__ inline void gate_up_row(const u32x4* __restrict__ wg, const u32x4* __
   if (lane == 0) upflag[row] = up ? 1 : 0;
 }
 
-// Optional phase timeline of the single-kernel path (compile with
-// -DSI_TRACE): per block, the 100 MHz real-time counter at numbered points.
+// Optional phase timeline of the single-kernel paths (compile with
+// -DSI_TRACE): per block (wave 0) and per wave, the 100 MHz real-time
+// counter at numbered points, held in registers and written out once at the
+// end of the kernel so that no store is in flight while the kernel runs.
 // Off in normal builds, where the marks compile to nothing.
 constexpr int kTraceSlots = 32;
+constexpr int kTraceBlockMarks = 12;
 constexpr int kTraceWaveMarks = 8;
 #ifdef SI_TRACE
 extern __device__ uint64_t g_si_trace[];
 extern __device__ uint64_t g_si_trace_wave[];
-#define SI_TRACE_MARK(slot)                                                                    \
-  do {                                                                                         \
-    if ((threadIdx.x & 63) == 0)                                                               \
-      g_si_trace[(size_t)blockIdx.x * kTraceSlots + (slot)] = __builtin_amdgcn_s_memrealtime(); \
-  } while (0)
-#define SI_TRACE_WAVE(mark)                                                                           \
-  do {                                                                                                \
-    if ((threadIdx.x & 63) == 0)                                                                      \
-      g_si_trace_wave[((size_t)blockIdx.x * 16 + (threadIdx.x >> 6)) * kTraceWaveMarks + (mark)] =   \
-          __builtin_amdgcn_s_memrealtime();                                                           \
+#define SI_TRACE_DECL                          \
+  uint64_t si_tr_[kTraceBlockMarks] = {};      \
+  uint64_t si_trw_[kTraceWaveMarks] = {}
+#define SI_TRACE_MARK(slot) (si_tr_[(slot)] = __builtin_amdgcn_s_memrealtime())
+#define SI_TRACE_WAVE(mark) (si_trw_[(mark)] = __builtin_amdgcn_s_memrealtime())
+#define SI_TRACE_FLUSH                                                                            \
+  do {                                                                                            \
+    if (threadIdx.x == 0)                                                                         \
+      for (int si_s_ = 0; si_s_ < kTraceBlockMarks; ++si_s_)                                      \
+        g_si_trace[(size_t)blockIdx.x * kTraceSlots + si_s_] = si_tr_[si_s_];                     \
+    if ((threadIdx.x & 63) == 0)                                                                  \
+      for (int si_m_ = 0; si_m_ < kTraceWaveMarks; ++si_m_)                                       \
+        g_si_trace_wave[((size_t)blockIdx.x * 16 + (threadIdx.x >> 6)) * kTraceWaveMarks + si_m_] = \
+            si_trw_[si_m_];                                                                       \
   } while (0)
 #else
+#define SI_TRACE_DECL \
+  do {                \
+  } while (0)
 #define SI_TRACE_MARK(slot) \
   do {                      \
   } while (0)
 #define SI_TRACE_WAVE(mark) \
   do {                      \
+  } while (0)
+#define SI_TRACE_FLUSH \
+  do {                 \
   } while (0)
 #endif
 

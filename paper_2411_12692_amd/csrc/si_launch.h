@@ -54,6 +54,12 @@ struct LayerCall {
 bool layer_supported(int k, int d, int b);
 hipError_t launch_layer(const LayerCall& c, hipStream_t s);
 
+// The row-owning single-launch kernel (owned.hip) for predict and mask
+// calls (idx_in must be NULL); idx, mask and n_out are each written when not
+// NULL.  Only valid when owned_supported(k, d, b).
+bool owned_supported(int k, int d, int b);
+hipError_t launch_owned(const LayerCall& c, hipStream_t s);
+
 // mask -> ascending kept list and count (single block).
 hipError_t launch_compact(const uint8_t* mask, int k, int32_t* idx, int32_t* n_out, hipStream_t s);
 
