@@ -38,8 +38,9 @@ def algorithmic_bytes(k, d, b, n_gate, n_up, n_down):
     return k * d // 8 + 2 * d * b + 2 * d * (n_gate + n_up + n_down) + 4 * d * b
 
 
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_layer_7b_s0.9_counters.txt")
-KERNEL_SOURCES = ("paper_2411_12692_amd/csrc/layer.hip", "paper_2411_12692_amd/csrc/si_device.h")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_7b_s0.9_counters.txt")
+KERNEL_SOURCES = ("paper_2411_12692_amd/csrc/owned.hip", "paper_2411_12692_amd/csrc/layer_common.h",
+                  "paper_2411_12692_amd/csrc/si_device.h")
 
 
 def kernel_sources_sha256():
@@ -53,7 +54,7 @@ def kernel_sources_sha256():
 
 
 def measured_traffic():
-    """HBM bytes per k_layer launch from the committed FETCH_SIZE/WRITE_SIZE
+    """HBM bytes per k_owned launch from the committed FETCH_SIZE/WRITE_SIZE
     summary, or None when that summary was taken on other kernel sources."""
     try:
         with open(COUNTERS_FILE) as f:
@@ -220,7 +221,7 @@ def main():
     print(f"# timed {steps} steps: {us_per_layer:.3f} us/layer (wall {wall * 1e6 / steps:.3f})",
           file=sys.stderr, flush=True)
 
-    # The timed graph holds nothing but k_layer launches on `stream`, so the
+    # The timed graph holds nothing but k_owned launches on `stream`, so the
     # per-step time above is that kernel's average launch duration.
     achieved = mean_bytes / us_per_layer / 1e3
 
@@ -261,7 +262,7 @@ def main():
             "bytes_per_layer": int(mean_bytes),
         },
         "roofline": {
-            "kernel": "k_layer (predict + compaction + gate/up + down, one launch per layer)",
+            "kernel": "k_owned (predict + group exchange + gate/up + down, one launch per layer)",
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,

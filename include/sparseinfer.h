@@ -157,10 +157,11 @@ si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint
 
 /*
  * 1 if si_predict, si_sparse_mlp and si_predict_sparse_mlp run as a single
- * kernel launch for these shapes on the current device: k <= 61440, b <= 8
- * (b <= 4 when d > 5120), and one 1024-thread block with 96-160 KB of LDS
- * resident on every compute unit; 0 if they take the multi-launch path (same
- * results) or the shapes are invalid.  Host-only query.
+ * kernel launch for these shapes on the current device: at most 256 rows of
+ * W_gate per compute unit (k <= 65536 on a 256-CU MI355X), b <= 8 (b <= 4
+ * when d > 5120), and one 1024-thread block with 96-160 KB of LDS resident
+ * on every compute unit; 0 if they take the multi-launch path (same results)
+ * or the shapes are invalid.  Host-only query.
  */
 int si_single_launch(int k, int d, int b);
 

@@ -1,57 +1,38 @@
-// The per-token MLP path of one layer in a single kernel: sign-bit
-// prediction (Section IV-A, Eq. (2)), the ordered list of kept rows, sparse
-// gate/up with actual sparsity and the sparse down-projection (Section IV-B
-// 3)-4)), for decode batches of up to 8 tokens.  The same kernel serves the
-// three calls of the boundary:
-//
-//  predict mode  the kept rows come from the packed signs (Eq. (2));
-//  mask mode     they come from a caller's mask;
-//  list mode     they come from a caller's ascending list and count;
-//
-// and, with the MLP switched off, the predictor alone.
+// The sparse gated MLP of one layer over a caller's list of kept rows in a
+// single kernel (si_sparse_mlp with an active list): sparse gate/up with
+// actual sparsity and the sparse down-projection (Section IV-B 3)-4)), for
+// decode batches of up to 8 tokens.  (Predict and mask calls take the
+// row-owning kernel of owned.hip.)
 //
 // One block of 16 wavefronts per compute unit, all blocks resident at once
 // (the host takes this path only when they fit; each block asks for more
 // than half of a CU's LDS so that no two share a CU).
 //
-//  1. predict   block b takes the 64-row groups b, b+P, ...: each wave
-//               XOR/popcounts its share of the group's 16-byte units (lane =
-//               row), wave 0 applies Eq. (2) as N_neg < T, writes the mask
-//               and publishes the group's kept mask and "confident" mask
-//               (N_neg < T - margin: almost surely active) as tagged words.
-//               In mask mode the kept mask is read from the caller's mask
-//               and every kept row counts as confident.
-//  2. exchange  every block reads the published masks of all groups (one
-//               poll per word, all in flight together) and forms the prefix
-//               of kept counts, so every block knows the whole ascending list
-//               of kept rows without a serial scan.  List mode skips steps 1
-//               and 2: the list is the caller's.
-//  3. plan      block b takes positions [n b / P, n (b+1) / P) of the list
-//               for gate/up (an even share whatever the groups' kept counts)
-//               and one down-projection item: 512-column tile (b mod T) of y
-//               and chunk (b / T) of the list.
-//  4. gate/up   in rounds of 8 rows, wave w owns (row w/2, W_gate or W_up)
-//               and requests all its 16-byte units at once.  W_up rows of
-//               confident rows are requested with W_gate; other rows read
-//               W_up only where some token's ReLU output is positive (actual
-//               sparsity).  h3 is published per list position and token.
-//  5. down      the tile's W_down^T pieces of the item's confident rows are
-//               requested once each wave's gate/up data is in; the item's h3
-//               words are collected, the remaining rows with non-zero h3 are
-//               fetched, the per-wave partial tiles are folded in LDS (plain
-//               stores) and the tile is added into y with fp32 atomics once
-//               the tile's owner has zeroed it in this call.
+//  1. plan      block b takes positions [n b / P, n (b+1) / P) of the list
+//               for gate/up (an even share) and one down-projection item:
+//               512-column tile (b mod T) of y and chunk (b / T) of the list.
+//  2. gate/up   in rounds of 8 rows, wave w owns (row w/2, W_gate or W_up)
+//               and requests all its 16-byte units at once.  W_up rows are
+//               requested with W_gate (given rows count as confident unless
+//               speculation is off); otherwise W_up is read only where some
+//               token's ReLU output is positive (actual sparsity).  h3 is
+//               published per list position and token.
+//  3. down      the tile's W_down^T pieces of the item's rows are requested
+//               once each wave's gate/up data is in; the item's h3 words are
+//               collected, the remaining rows with non-zero h3 are fetched,
+//               the per-wave partial tiles are folded in LDS (plain stores)
+//               and the tile is added into y with fp32 atomics once the
+//               tile's owner has zeroed it in this call.
 //
 // Blocks exchange data through 64-bit words: the high half is this call's
 // tag (the workspace's call counter with the high bit set), the low half the
 // payload.  They are written with agent-scope write-through stores and read
 // with agent-scope loads; a word is valid once it carries the call's tag, so
 // no cache flush or fence is needed and the workspace is never cleared
-// between calls.  Block 0 advances the call counter once it has seen a word
-// of this call from every block (its group's masks, or an "alive" word from
-// blocks without a group and in list mode), i.e. once every block has read
-// it.  Every wait is bounded: past a spin limit the block sets an error bit
-// in the workspace header and goes on without the data.
+// between calls.  Block 0 advances the call counter once it has seen every
+// block's "alive" word, i.e. once every block has read it.  Every wait is
+// bounded: past a spin limit the block sets an error bit in the workspace
+// header and goes on without the data.
 
 #include "layer_common.h"
 
@@ -68,34 +49,24 @@ extern "C" hipError_t si_trace_wave_read(void* dst, size_t bytes) {
 }
 #endif
 
-constexpr int kMaxLayerGroups = 960;       // masks of every group are held in LDS (k <= 61440)
-constexpr int kMaxPollWords = 4 * kLThreads;
 constexpr int kMaxSlice = 256;             // gate/up positions of one block (at most)
-enum : int { kModePredict = 0, kModeMask = 1, kModeList = 2 };
 
 struct LayerArgs {
-  const u32x4* signs;
   const u32x4* wg;
   const u32x4* wu;
   const u32x4* wdt;
   const uint16_t* x;
-  const uint8_t* mask_in;  // mask mode
-  const int32_t* idx_in;   // list mode
-  const int32_t* n_in;     // list mode
-  int k, d, b, T, margin;
+  const int32_t* idx_in;  // the caller's ascending kept rows
+  const int32_t* n_in;    // and their count (device)
+  int k, d, b;
   uint32_t flags;
-  int mode, mlp;
-  uint8_t* mask;    // predict mode: written
-  int32_t* idx;     // predict and mask modes: written
-  int32_t* n_out;   // predict and mask modes: written
   uint32_t* hdr;
-  uint64_t* pub;    // [groups][4] tag | kept mask low/high half, tag | confident mask low/high half
   uint64_t* h3e;    // [k][b] tag | fp32 bits of h3, by list position and token
   uint64_t* zflag;  // [tiles] tag once the tile of y is zero
-  uint64_t* alive;  // [blocks] tag, from blocks that publish no group (all blocks in list mode)
+  uint64_t* alive;  // [blocks] tag once the block has read the call counter
   int32_t* counts;  // [blocks][2] W_up rows read, W_down^T rows read (tile-0 items)
   float* y;
-  int groups, tiles, chunks;
+  int tiles, chunks;
   double inv_blocks, inv_chunks;  // 1 / grid size, 1 / chunks (exact floors of n b / P, n c / C)
 };
 
@@ -111,18 +82,6 @@ struct LayerLds {
     u32x4 xs[BM * kUnits];
     float dpart[kFold][BM][kTile];
   };
-  uint32_t xw[BM * kUnits / 4];  // sign words of the tokens
-  // per-wave N_neg partial counts during the prediction; the published masks
-  // of every group and their prefix afterwards
-  union {
-    int cpart[kLWaves][BM][kWave];
-    struct {
-      uint32_t pm[4 * kMaxLayerGroups];
-      int pre[kMaxLayerGroups];
-    } ex;
-  };
-  int wtot[kLWaves];
-  int gfirst[2];                  // group holding the first position of the slice / the down item
   float dots[kRoundRows][2][BM];  // W_gate . x and W_up . x of the round's rows
   float h1[kRoundRows][BM];
   uint32_t need[kRoundRows];      // round row needs a late W_up read
@@ -146,31 +105,19 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
   LayerLds<BM, NU>& L = *reinterpret_cast<LayerLds<BM, NU>*>(lds_raw);
 
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int d = a.d, U = d >> 3, W = d >> 5, units = d >> 7;
+  const int d = a.d, U = d >> 3;
   const int b = a.b;  // tokens, 1..BM; tokens b..BM-1 are zero
-  const int P = gridDim.x, blk = blockIdx.x, G = a.groups;
+  const int P = gridDim.x, blk = blockIdx.x;
   const int T = a.tiles;
-  const int mode = a.mode;
   const bool no_as = (a.flags & kNoAS) != 0;
   const bool spec_ok = (a.flags & kNoSpec) == 0;
 
   SI_TRACE_DECL;
   SI_TRACE_MARK(0);
-  // ---- the packed signs of the block's first group are requested, then
-  // the tokens and (behind the first token requests, so that the wait for
-  // it, which comes at once for an atomic load, also covers them) the call
-  // counter; addresses are clamped so that the requests are unconditional
-  // and go out back to back; tokens b..BM-1 are zero
-  u32x4 sreg[kMaxSignUnitsPerWave];
-  auto load_signs = [&](int g) {
-    const u32x4* sg = a.signs + (size_t)g * units * kRowGroup + lane;
-#pragma unroll
-    for (int i = 0; i < kMaxSignUnitsPerWave; ++i) {
-      const int q = wv + kLWaves * i;
-      if (q < units) sreg[i] = load_nt(sg + (size_t)q * kRowGroup);
-    }
-  };
-  if (mode == kModePredict && blk < G) load_signs(blk);
+  // ---- the tokens and (behind the first token requests, so that the wait
+  // for it, which comes at once for an atomic load, also covers them) the
+  // call counter; addresses are clamped so that the requests are
+  // unconditional and go out back to back; tokens b..BM-1 are zero
   {
     const u32x4* xg = reinterpret_cast<const u32x4*>(a.x);
     const int nx = b * U;
@@ -186,151 +133,28 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
       L.xs[i] = i < nx ? xv : u32x4{0, 0, 0, 0};
     }
   }
-  __syncthreads();
-  const uint32_t epoch = uniform(L.epoch);
-  const uint32_t tag = epoch_tag(epoch);
-  if (tid == 0 && (mode == kModeList || blk >= G))  // this block has read the call counter
-    st_agent64(&a.alive[blk], tagged(tag, 0u));
-  if (mode == kModePredict) {
-    for (int i = tid; i < b * W; i += kLThreads) {
-      const int t = i / W, w = i - t * W;
-      L.xw[i] = sign_word(&L.xs[t * U + 4 * w]);
-    }
-  }
-  __syncthreads();
-  SI_TRACE_MARK(1);
-
-  // ---- 1. the kept and confident rows of the block's groups
-  if (mode != kModeList) {
-    for (int g = blk; g < G; g += P) {
-      if (mode == kModePredict) {
-        if (g != blk) load_signs(g);
-        int c[BM];
-#pragma unroll
-        for (int t = 0; t < BM; ++t) c[t] = 0;
-        bool any_unit = false;
-#pragma unroll
-        for (int i = 0; i < kMaxSignUnitsPerWave; ++i) {
-          const int q = wv + kLWaves * i;
-          if (q < units) {
-            any_unit = true;
-#pragma unroll
-            for (int t = 0; t < BM; ++t) {
-              if (t < b) {
-                const u32x4 xv = *reinterpret_cast<const u32x4*>(&L.xw[t * W + 4 * q]);
-                c[t] += __popc(sreg[i].x ^ xv.x) + __popc(sreg[i].y ^ xv.y) + __popc(sreg[i].z ^ xv.z) +
-                        __popc(sreg[i].w ^ xv.w);
-              }
-            }
-          }
-        }
-        if (any_unit) {
-#pragma unroll
-          for (int t = 0; t < BM; ++t)
-            if (t < b) L.cpart[wv][t][lane] = c[t];
-        }
-        __syncthreads();
-      }
-      if (wv == 0) {
-        const int row = g * kRowGroup + lane;
-        bool keep = false, conf = false;
-        if (mode == kModePredict) {
-          const int nw = min(units, kLWaves);  // waves that counted units
-#pragma unroll
-          for (int t = 0; t < BM; ++t) {
-            if (t < b) {
-              int n_neg = 0;
-              for (int w = 0; w < nw; ++w) n_neg += L.cpart[w][t][lane];
-              keep |= n_neg < a.T;
-              conf |= n_neg < a.T - a.margin;
-            }
-          }
-          keep = keep && row < a.k;
-          if (row < a.k) a.mask[row] = keep ? 1 : 0;
-        } else {  // mask mode: every kept row is treated as confident
-          keep = row < a.k && a.mask_in[row] != 0;
-          conf = keep;
-        }
-        const uint64_t kb = __ballot(keep);
-        const uint64_t cb = __ballot(keep && conf);
-        if (lane < 4) {
-          const uint64_t m = lane < 2 ? kb : cb;
-          st_agent64(&a.pub[(size_t)g * 4 + lane], tagged(tag, (uint32_t)(m >> (32 * (lane & 1)))));
-        }
-      }
-      __syncthreads();
-    }
-  }
-  // the tile of y this block owns is zeroed while the masks are exchanged
-  const bool owns_tile = a.mlp && blk < T;
+  // the tile of y this block owns is zeroed (announced after the plan)
+  const bool owns_tile = blk < T;
   if (owns_tile) {
     for (int i = tid; i < b * kTile; i += kLThreads) {
       const int t = i / kTile, col = blk * kTile + (i - t * kTile);
       if (col < d) __hip_atomic_store(&a.y[(size_t)t * d + col], 0.f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
-  SI_TRACE_MARK(2);
-
-  // ---- 2. every group's masks and the words of the blocks without a group;
-  // then block 0 knows every block has read the call counter and advances it
-  if (mode != kModeList) {
-    const int NWp = 4 * G;
-    const int NW = NWp + (P > G ? P - G : 0);
-    uint64_t v[kMaxPollWords / kLThreads];
-    uint32_t pending = 0;
-#pragma unroll
-    for (int i = 0; i < kMaxPollWords / kLThreads; ++i) {
-      const int j = tid + kLThreads * i;
-      if (j < NW) pending |= 1u << i;
-    }
-    long spins = 0;
-    while (pending) {
-#pragma unroll
-      for (int i = 0; i < kMaxPollWords / kLThreads; ++i) {
-        const int j = tid + kLThreads * i;
-        if ((pending >> i) & 1u) v[i] = ld_agent64(j < NWp ? &a.pub[j] : &a.alive[G + (j - NWp)]);
-      }
-#pragma unroll
-      for (int i = 0; i < kMaxPollWords / kLThreads; ++i) {
-        const int j = tid + kLThreads * i;
-        if (((pending >> i) & 1u) && (uint32_t)(v[i] >> 32) == tag) {
-          if (j < NWp) L.ex.pm[j] = (uint32_t)v[i];
-          pending &= ~(1u << i);
-        }
-      }
-      if (pending) {
-        if (++spins > kPollLimit) {
-          atomicOr(&a.hdr[H_ERR], kErrLookbackSpin);
-#pragma unroll
-          for (int i = 0; i < kMaxPollWords / kLThreads; ++i) {
-            const int j = tid + kLThreads * i;
-            if (((pending >> i) & 1u) && j < NWp) L.ex.pm[j] = 0u;
-          }
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-      }
-    }
-  }
-  // every load of this wave has been consumed by now; waiting here (at no
-  // cost) also tells the compiler so, and it then issues the gate/up row
-  // requests back to back (without waits between them); owners also know
-  // their y-zeroing stores have landed
-  wait_own_stores();
   __syncthreads();
-  if (tid == 0) {
-    if (owns_tile) st_agent64(&a.zflag[blk], tagged(tag, 1u));
-    if (mode != kModeList && blk == 0) advance_epoch(a.hdr, epoch);
-  }
-  SI_TRACE_MARK(3);
+  const uint32_t epoch = uniform(L.epoch);
+  const uint32_t tag = epoch_tag(epoch);
+  if (tid == 0) st_agent64(&a.alive[blk], tagged(tag, 0u));  // this block has read the call counter
+  SI_TRACE_MARK(1);
 
-  // ---- 3. plan: the block's gate/up slice and down item, and the list
+  // ---- 1. plan: the block's gate/up slice and down item, and the list
   // entries that fall in them
   const int C = a.chunks;
-  const bool has_item = a.mlp && blk < T * C;
+  const bool has_item = blk < T * C;
   const int tile = has_item ? blk % T : 0, chunk = has_item ? blk / T : 0;
-  if (mode == kModeList) {
+  {
     const int n = min(max(*a.n_in, 0), a.k);
+    // floor(n b / P) etc.: (x + 1/2) / P is at least 1 / (2P) away from an integer
     const int lo_ = (int)(((double)n * blk + 0.5) * a.inv_blocks);
     const int hi_ = (int)(((double)n * (blk + 1) + 0.5) * a.inv_blocks);
     const int dlo_ = has_item ? (int)(((double)n * chunk + 0.5) * a.inv_chunks) : 0;
@@ -353,74 +177,17 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
       L.sc[3] = dlo_;
       L.sc[4] = dhi_;
     }
-  } else {
-    // kept count of every group (one group per thread) and their block-wide
-    // prefix; then one wave per group that holds positions of the block's
-    // ranges writes their list entries (lane = row: rank among the kept rows)
-    uint64_t km = 0;
-    if (tid < G) km = (uint64_t)L.ex.pm[4 * tid] | ((uint64_t)L.ex.pm[4 * tid + 1] << 32);
-    const int c = __popcll(km);
-    const int incl = wave_incl_scan(c);
-    if (lane == kWave - 1) L.wtot[wv] = incl;
-    if (tid < 2) L.gfirst[tid] = G;
-    __syncthreads();
-    const int wt = wave_incl_scan(lane < kLWaves ? L.wtot[lane] : 0);  // lanes 0..15: prefix of wave totals
-    const int n = uniform(__builtin_amdgcn_readlane(wt, kLWaves - 1));
-    const int before = wv > 0 ? uniform(__builtin_amdgcn_readlane(wt, wv > 0 ? wv - 1 : 0)) : 0;
-    // floor(n b / P) etc.: (x + 1/2) / P is at least 1 / (2P) away from an integer
-    const int lo_ = (int)(((double)n * blk + 0.5) * a.inv_blocks);
-    const int hi_ = (int)(((double)n * (blk + 1) + 0.5) * a.inv_blocks);
-    const int dlo_ = has_item ? (int)(((double)n * chunk + 0.5) * a.inv_chunks) : 0;
-    const int dhi_ = has_item ? (int)(((double)n * (chunk + 1) + 0.5) * a.inv_chunks) : 0;
-    const int pi = before + incl, pe = pi - c;  // the group's kept rows hold positions [pe, pi)
-    if (tid < G) {
-      L.ex.pre[tid] = pi;
-      if (lo_ < hi_ && pe <= lo_ && lo_ < pi) L.gfirst[0] = tid;
-      if (dlo_ < dhi_ && pe <= dlo_ && dlo_ < pi) L.gfirst[1] = tid;
-    }
-    if (tid == 0) {
-      L.sc[1] = lo_;
-      L.sc[2] = hi_;
-      L.sc[3] = dlo_;
-      L.sc[4] = dhi_;
-      if (blk == 0) *a.n_out = n;
-    }
-    __syncthreads();
-    // waves 0..7: groups from the slice's first; waves 8..15: from the down item's first
-    const bool down_side = wv >= kLWaves / 2;
-    const int rlo = down_side ? dlo_ : lo_, rhi = down_side ? dhi_ : hi_;
-    for (int g = uniform(L.gfirst[down_side ? 1 : 0]) + (wv & 7); g < G; g += kLWaves / 2) {
-      const int gpi = L.ex.pre[g];
-      const uint64_t gk = (uint64_t)L.ex.pm[4 * g] | ((uint64_t)L.ex.pm[4 * g + 1] << 32);
-      const int gpe = gpi - __popcll(gk);
-      if (gpe >= rhi) break;
-      if (gpi <= rlo) continue;
-      const uint64_t gc = (uint64_t)L.ex.pm[4 * g + 2] | ((uint64_t)L.ex.pm[4 * g + 3] << 32);
-      const int q = gpe + __popcll(gk & lanes_below(lane));
-      if (((gk >> lane) & 1ull) && q >= rlo && q < rhi) {
-        const uint32_t e = (uint32_t)(g * kRowGroup + lane) | (((gc >> lane) & 1ull) ? 0x80000000u : 0u);
-        if (down_side) {
-          L.dent[q - rlo] = e;
-        } else {
-          L.srow[q - rlo] = e;
-          a.idx[q] = g * kRowGroup + lane;
-        }
-      }
-    }
   }
+  // every load of this wave has been consumed by now; waiting here (at no
+  // cost) also tells the compiler so, and it then issues the gate/up row
+  // requests back to back (without waits between them); owners also know
+  // their y-zeroing stores have landed
+  wait_own_stores();
   __syncthreads();
+  if (tid == 0 && owns_tile) st_agent64(&a.zflag[blk], tagged(tag, 1u));
   const int lo = uniform(L.sc[1]), hi = uniform(L.sc[2]);
   const int dlo = uniform(L.sc[3]), dhi = uniform(L.sc[4]);
   SI_TRACE_MARK(4);
-  if (!a.mlp) {  // the predictor alone
-    if (tid == 0) {
-      a.counts[2 * blk] = 0;
-      a.counts[2 * blk + 1] = 0;
-    }
-    SI_TRACE_FLUSH;
-    return;
-  }
-
   // ---- down requests of a round: this wave's positions q0 + wv + 16 j
   u32x4 vd[kDN];
   uint32_t dloaded = 0;
@@ -522,7 +289,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) acc[t][q] = 0.f;
   int n_down = 0;
-  bool epoch_done = mode != kModeList;
+  bool epoch_done = false;
   for (int q0 = dlo; q0 < dhi; q0 += kDownRound) {
     const int nq = min(kDownRound, dhi - q0);
     if (q0 != dlo) {
@@ -531,7 +298,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
     }
     // waves 0..3 collect the round's h3 words (contiguous: positions x
     // tokens, all requests in flight together); in the first round wave 4
-    // checks the tile's zero flag and, in list mode, waves 8.. of block 0
+    // checks the tile's zero flag and waves 8.. of block 0
     // collect every block's alive word
     if (tid < kDownPollThreads) {
       constexpr int kPer = (kDownRound * BM + kDownPollThreads - 1) / kDownPollThreads;
@@ -649,7 +416,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
       if (col < d && v != 0.f) unsafeAtomicAdd(&a.y[(size_t)t * d + col], v);
     }
   }
-  if (!epoch_done && blk == 0) {  // list mode without a down round
+  if (!epoch_done && blk == 0) {  // no down round in block 0
     wait_alive(a.alive, P, tid, kLThreads, tag, a.hdr);
     __syncthreads();
     if (tid == 0) advance_epoch(a.hdr, epoch);
@@ -727,41 +494,30 @@ static hipError_t layer_b(const LayerCall& c, hipStream_t s) {
     const int P = layer_blocks<BM, NU>();
     if (P < 1) return hipErrorInvalidConfiguration;
     LayerArgs a;
-    a.signs = reinterpret_cast<const u32x4*>(c.signs);
     a.wg = reinterpret_cast<const u32x4*>(c.w_gate);
     a.wu = reinterpret_cast<const u32x4*>(c.w_up);
     a.wdt = reinterpret_cast<const u32x4*>(c.w_down_t);
     a.x = c.x;
-    a.mask_in = c.mask_in;
     a.idx_in = c.idx_in;
     a.n_in = c.n_in;
     a.k = k;
     a.d = d;
     a.b = c.b;
-    a.T = c.T;
-    a.margin = c.margin;
     a.flags = c.flags;
-    a.mode = c.idx_in ? kModeList : c.mask_in ? kModeMask : kModePredict;
-    a.mlp = c.y != nullptr;
-    a.mask = c.mask;
-    a.idx = c.idx;
-    a.n_out = c.n_out;
     a.hdr = reinterpret_cast<uint32_t*>(base);
-    a.pub = reinterpret_cast<uint64_t*>(base + L.lmask);
     a.zflag = reinterpret_cast<uint64_t*>(base + L.zflag);
     a.alive = reinterpret_cast<uint64_t*>(base + L.alive);
     a.h3e = reinterpret_cast<uint64_t*>(base + L.h3e);
     a.counts = reinterpret_cast<int32_t*>(base + L.counts);
     a.y = c.y;
-    a.groups = row_groups(k);
     a.tiles = (d + kTile - 1) / kTile;
     a.chunks = P / a.tiles;
     a.inv_blocks = 1.0 / P;
     a.inv_chunks = 1.0 / a.chunks;
     k_layer<BM, NU><<<P, kLThreads, layer_lds_bytes<BM, NU>(), s>>>(a);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !c.counters || !c.y) return e;
-    return launch_sum_counts(a.counts, P, c.idx_in ? c.n_in : c.n_out, k, c.counters, s);
+    if (e != hipSuccess || !c.counters) return e;
+    return launch_sum_counts(a.counts, P, c.n_in, k, c.counters, s);
   }
 }
 
@@ -772,17 +528,14 @@ static int blocks_for(int d, int b) {
 #undef BLOCKS
 }
 
-// The single-kernel path applies up to kMaxLayerGroups row groups (every
-// group's masks fit in LDS and in one poll per thread) and when one block per
-// CU can be resident with the LDS that the batch and row width need.
+// The list kernel applies when one block per CU can be resident with the
+// LDS that the batch and row width need, and a block's gate/up slice and
+// down item fit their LDS lists.
 bool layer_supported(int k, int d, int b) {
-  const int G = row_groups(k);
-  if (G > kMaxLayerGroups) return false;
   const int P = blocks_for(d, b);
   const int tiles = (d + kTile - 1) / kTile;
-  if (P < tiles) return false;
+  if (P < 1 || P < tiles) return false;
   const int chunks = P / tiles;
-  if (4 * G + (P > G ? P - G : 0) > kMaxPollWords) return false;
   return (k + P - 1) / P <= kMaxSlice && (k + chunks - 1) / chunks <= kMaxDownItem;
 }
 

@@ -198,13 +198,13 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
   // them) the call counter; addresses are clamped so that the requests are
   // unconditional and go out back to back; tokens b..BM-1 are zero
   u32x4 sreg[kMaxSignUnitsPerWave];
+  const int kpad = (k + kRowGroup - 1) / kRowGroup * kRowGroup;  // rows of the packed layout
   auto load_signs = [&](int s) {
-    const int rr = r0 + min(s * kWave + lane, Rb - 1);
-    const u32x4* sg = a.signs + (size_t)(rr >> 6) * units * kRowGroup + (rr & (kRowGroup - 1));
+    const u32x4* sg = a.signs + r0 + min(s * kWave + lane, Rb - 1);
 #pragma unroll
     for (int i = 0; i < kMaxSignUnitsPerWave; ++i) {
       const int q = wv + kLWaves * i;
-      if (q < units) sreg[i] = load_nt(sg + (size_t)q * kRowGroup);
+      if (q < units) sreg[i] = load_nt(sg + (size_t)q * kpad);
     }
   };
   uint32_t mbyte = 0;
@@ -668,6 +668,15 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
   SI_TRACE_FLUSH;
 }
 
+// Rows per block: the rows spread over the whole groups of the grid,
+// rounded up to a multiple of 8 so that a block's piece of each sign unit
+// (R * 16 bytes) starts and ends on a 128-byte line.
+static int owned_rows_per_block(int k, int P, int tiles) {
+  const int working = P / tiles * tiles;
+  const int R = (k + working - 1) / working;
+  return (R + 7) / 8 * 8;
+}
+
 template <int BM, int NU>
 static int owned_blocks() {
   static int blocks = -1;
@@ -712,8 +721,8 @@ static hipError_t owned_b(const LayerCall& c, hipStream_t s) {
     a.flags = c.flags;
     a.mlp = c.y != nullptr;
     a.tiles = (d + kTile - 1) / kTile;
-    a.groups = P / a.tiles;
-    a.R = (k + a.groups * a.tiles - 1) / (a.groups * a.tiles);
+    a.R = owned_rows_per_block(k, P, a.tiles);
+    a.groups = min(P / a.tiles, (k + a.R * a.tiles - 1) / (a.R * a.tiles));
     a.nsub = (a.R + kWave - 1) / kWave;
     a.mask = c.mask;
     a.idx = c.idx;
@@ -746,8 +755,7 @@ bool owned_supported(int k, int d, int b) {
   const int P = owned_blocks_for(d, b);
   const int tiles = (d + kTile - 1) / kTile;
   if (P < 1 || P < tiles) return false;
-  const int working = P / tiles * tiles;  // blocks that own rows
-  const int R = (k + working - 1) / working;
+  const int R = owned_rows_per_block(k, P, tiles);
   if (R > kMaxOwnRows) return false;
   const int nsub = (R + kWave - 1) / kWave;
   return tiles * nsub <= kMaxPairs && tiles * R <= kMaxChunkRows;

@@ -1,21 +1,21 @@
 // Load-time preprocessing: sign packing of W_gate (Section IV-B 1) and the
 // transpose of W_down (Section IV-B 4).
 //
-// Packed-sign layout (private to the library).  Rows are taken in groups of
-// 64; inside a group the 32-bit words are stored unit-major, where a unit is
-// 4 consecutive words (128 elements) of one row:
-//     word (row i, w) -> [group i/64][unit w/4][row i%64][w%4]
-// so that one wavefront reading unit q of its 64 rows touches 1 KB of
-// contiguous memory with one 16-byte load per lane (lane = row).  Bit j of
-// word w is the sign of element 32*w + j.  Padding rows are all zero.
+// Packed-sign layout (private to the library).  A unit is 4 consecutive
+// 32-bit words (128 elements) of one row; units are stored unit-major over
+// the rows, which are padded to a multiple of 64 (kpad):
+//     word (row i, w) -> [unit w/4][row i][w%4]
+// so that unit q of any run of consecutive rows is one contiguous piece of
+// memory, read with one 16-byte load per lane (lane = row): 1 KB for a
+// 64-row group, R * 16 bytes for a block's R rows.  Bit j of word w is the
+// sign of element 32*w + j.  Padding rows are all zero.
 #include "si_device.h"
 #include "si_launch.h"
 
 namespace si {
 
-__device__ inline size_t packed_index(int i, int w, int units) {
-  const int g = i >> 6, r = i & 63, q = w >> 2, j = w & 3;
-  return (((size_t)g * units + q) * kRowGroup + r) * 4 + j;
+__device__ inline size_t packed_index(int i, int w, int kpad) {
+  return ((size_t)(w >> 2) * kpad + i) * 4 + (w & 3);
 }
 
 // One thread per (row, word): reads 32 consecutive fp16 (64 bytes; adjacent
@@ -29,16 +29,17 @@ __global__ __launch_bounds__(256) void k_pack_signs(const uint16_t* __restrict__
   const int i = (int)(t / W), wd = (int)(t % W);
   uint32_t word = 0;
   if (i < k) word = sign_word(reinterpret_cast<const u32x4*>(w + (size_t)i * d + 32 * wd));
-  signs[packed_index(i, wd, W >> 2)] = word;
+  signs[packed_index(i, wd, kpad)] = word;
 }
 
 __global__ __launch_bounds__(256) void k_signs_to_canonical(const uint32_t* __restrict__ signs, int k,
                                                             int d, uint32_t* __restrict__ out) {
   const int W = d >> 5;
+  const int kpad = (k + kRowGroup - 1) / kRowGroup * kRowGroup;
   const size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (size_t)k * W) return;
   const int i = (int)(t / W), wd = (int)(t % W);
-  out[t] = signs[packed_index(i, wd, W >> 2)];
+  out[t] = signs[packed_index(i, wd, kpad)];
 }
 
 // out[c][r] = in[r][c] for a rows x cols fp16 matrix, 64x64 tiles through LDS.

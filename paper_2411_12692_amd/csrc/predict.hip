@@ -104,10 +104,11 @@ __global__ __launch_bounds__(kPredWaves * kWave) void k_rows(
   int c[B];
 #pragma unroll
   for (int t = 0; t < B; ++t) c[t] = 0;
-  const u32x4* sg = signs + (size_t)v * units * kRowGroup + lane;
+  const int kpad = groups * kRowGroup;  // rows of the packed layout (unit q of row i at q * kpad + i)
+  const u32x4* sg = signs + (size_t)v * kRowGroup + lane;
 #pragma unroll 4
   for (int q = wv; q < units; q += kPredWaves) {
-    const u32x4 s = load_nt(sg + (size_t)q * kRowGroup);
+    const u32x4 s = load_nt(sg + (size_t)q * kpad);
 #pragma unroll
     for (int t = 0; t < B; ++t) {
       const u32x4 xv = *reinterpret_cast<const u32x4*>(&xw[t * W + 4 * q]);

@@ -278,9 +278,9 @@ def test_batch_union(b):
 
 
 @pytest.mark.parametrize("k,d", [(1, 128), (63, 128), (65, 384), (129, 8192), (1000, 640), (1, 8192),
-                                 (20000, 384), (61440, 128)])
+                                 (20000, 384), (65536, 128)])
 def test_sparse_mlp_edge_shapes(k, d):
-    """Ragged tails of rows, pieces and tiles; k = 20000 and 61440 give more
+    """Ragged tails of rows, pieces and tiles; k = 20000 and 65536 give more
     64-row groups than there are blocks (several groups per block)."""
     rng = np.random.default_rng(k * 17 + d)
     c = Case(rand_bits(rng, (k, d), False), rand_bits(rng, (k, d), False), rand_bits(rng, (d, k), False),
@@ -327,13 +327,14 @@ def test_13b_layer():
 
 
 @pytest.mark.parametrize("k,d,b,one", [(11008, 4096, 1, 1), (13824, 5120, 1, 1), (1376, 512, 1, 1),
-                                       (11008, 4096, 2, 1), (1, 128, 1, 1), (61440, 128, 1, 1),
+                                       (11008, 4096, 2, 1), (1, 128, 1, 1), (65536, 128, 1, 1),
                                        (11008, 4096, 3, 1), (11008, 4096, 8, 1), (13824, 5120, 8, 1),
-                                       (129, 8192, 4, 1), (129, 8192, 5, 0), (61441, 128, 1, 0),
+                                       (129, 8192, 4, 1), (129, 8192, 5, 0), (65537, 128, 1, 0),
                                        (11008, 4096, 9, 0)])
 def test_single_launch_path(k, d, b, one):
     """The shapes the parity tests use run the one-launch kernel (so its
-    results are the ones checked); k above 61440 and batches of more than 4
+    results are the ones checked); k above 65536 (256 rows per compute unit)
+    and batches of more than 4
     tokens at d > 5120 take the two-launch path."""
     assert si._lib.load().si_single_launch(k, d, b) == one
 
