@@ -36,7 +36,7 @@ import torch
 
 _TENSOR_IDS = {
     "x": 0, "perm": 1, "disagree": 2, "gate_mag": 3, "up": 4, "down": 5,
-    "noise": 6, "ref_sign": 7, "tokens": 8, "token_sets": 9, "sparsity": 10,
+    "noise": 6, "ref_sign": 7, "tokens": 8, "token_sets": 9, "sparsity": 10, "calib": 11,
 }
 
 
@@ -82,13 +82,16 @@ class PlantedLayer:
 
 
 def planted_gate(d: int, k: int, s: float, ref_negative: torch.Tensor,
-                 config: int, layer: int, device="cpu"):
+                 config: int, layer: int, device="cpu", p_active: float = 0.4, p_inactive: float = 0.6):
     """``W_gate [k][d]`` fp16 planted against the sign pattern ``ref_negative``
-    (``[d]`` bool, True = negative), plus the ``[k]`` bool inactive set."""
+    (``[d]`` bool, True = negative), plus the ``[k]`` bool inactive set.
+    Elements disagree in sign with the pattern with probability ``p_active``
+    on active rows and ``p_inactive`` on inactive rows (0.4 / 0.6 by default;
+    values closer to 0.5 make the sign-bit prediction less certain)."""
     perm = torch.randperm(k, generator=generator(config, layer, "perm", device), device=device)
     inactive = torch.zeros(k, dtype=torch.bool, device=device)
     inactive[perm[: n_inactive(k, s)]] = True
-    p_disagree = torch.where(inactive, 0.6, 0.4).to(device)
+    p_disagree = torch.where(inactive, p_inactive, p_active).to(device)
     coins = torch.rand(k, d, generator=generator(config, layer, "disagree", device), device=device)
     disagree = coins < p_disagree[:, None]
     del coins
@@ -104,11 +107,11 @@ def normal_fp16(shape, std: float, config: int, layer: int, tensor: str, device=
 
 
 def planted_layer(d: int, k: int, s: float, config: int = 1, layer: int = 0,
-                  device="cpu") -> PlantedLayer:
+                  device="cpu", p_active: float = 0.4, p_inactive: float = 0.6) -> PlantedLayer:
     """Single-token layer of the planted construction (see module docstring)."""
     x = normal_fp16((1, d), 1.0, config, layer, "x", device)
     x_negative = x[0].view(torch.int16) < 0
-    w_gate, inactive = planted_gate(d, k, s, x_negative, config, layer, device)
+    w_gate, inactive = planted_gate(d, k, s, x_negative, config, layer, device, p_active, p_inactive)
     w_up = normal_fp16((k, d), 0.02, config, layer, "up", device)
     w_down = normal_fp16((d, k), 0.02, config, layer, "down", device)
     return PlantedLayer(d, k, s, x, w_gate, w_up, w_down, inactive)
@@ -152,12 +155,13 @@ def reference_signs(d: int, config: int, layer: int, device="cpu") -> torch.Tens
     return torch.rand(d, generator=g, device=device) < 0.5
 
 
-def stack_layer(d: int, k: int, s: float, config: int, layer: int, device="cpu"):
+def stack_layer(d: int, k: int, s: float, config: int, layer: int, device="cpu",
+                p_active: float = 0.4, p_inactive: float = 0.6):
     """Layer ``layer`` of a planted stack: gate rows planted against
     :func:`reference_signs` of that layer.  Returns ``(w_gate, w_up, w_down,
     inactive, ref_negative)``."""
     ref = reference_signs(d, config, layer, device)
-    w_gate, inactive = planted_gate(d, k, s, ref, config, layer, device)
+    w_gate, inactive = planted_gate(d, k, s, ref, config, layer, device, p_active, p_inactive)
     w_up = normal_fp16((k, d), 0.02, config, layer, "up", device)
     w_down = normal_fp16((d, k), 0.02, config, layer, "down", device)
     return w_gate, w_up, w_down, inactive, ref
@@ -195,3 +199,14 @@ def stack_input(y_prev, d: int, b: int, config: int, layer: int, token: int, dev
         mag = (y / rms + eps).abs()
     neg = reference_signs(d, config, layer, device)
     return fp16_with_sign(mag, neg[None, :].expand(b, d))
+
+
+def calibration_tokens(d: int, n: int, config: int, layer: int, flip: float = 0.0, device="cpu") -> torch.Tensor:
+    """``[n][d]`` fp16 tokens for calibrating a stacked layer: magnitudes
+    ``|N(0, 1)|``, signs the layer's reference pattern with each sign flipped
+    independently with probability ``flip`` (0 keeps the planted relation)."""
+    g = generator(config, layer, "calib", device)
+    mag = torch.randn(n, d, generator=g, device=device).abs()
+    flips = torch.rand(n, d, generator=g, device=device) < flip
+    neg = reference_signs(d, config, layer, device)[None, :] ^ flips
+    return fp16_with_sign(mag, neg)
