@@ -119,10 +119,13 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
   // call counter; addresses are clamped so that the requests are
   // unconditional and go out back to back; tokens b..BM-1 are zero
   {
+    // token t's unit u at xs[t * XS + u] (XS = NU * 64 >= U)
+    constexpr int XS = LayerLds<BM, NU>::kUnits;
     const u32x4* xg = reinterpret_cast<const u32x4*>(a.x);
     const int nx = b * U;
-    for (int i = tid; i < BM * U; i += kLThreads) {
-      const u32x4 xv = xg[min(i, nx - 1)];
+    for (int i = tid; i < BM * XS; i += kLThreads) {
+      const int t = i / XS, u = i - t * XS;
+      const u32x4 xv = xg[min(t * U + u, nx - 1)];
       if (i == tid && tid == 0) {
         asm volatile("" ::: "memory");
         L.epoch = ld_agent(&a.hdr[H_EPOCH]);
@@ -130,7 +133,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
         L.n_down = 0;
         L.zok = 0;
       }
-      L.xs[i] = i < nx ? xv : u32x4{0, 0, 0, 0};
+      L.xs[i] = (t < b && u < U) ? xv : u32x4{0, 0, 0, 0};
     }
   }
   // the tile of y this block owns is zeroed (announced after the plan)

@@ -111,7 +111,9 @@ __device__ inline void wait_alive(const uint64_t* alive, int blocks, int t, int 
 __device__ inline void advance_epoch(uint32_t* hdr, uint32_t epoch) { st_agent(&hdr[H_EPOCH], epoch + 1u); }
 
 // Dot products of a row held as NU 16-byte units per lane (unit lane + 64 j)
-// with the BM tokens in LDS; wave-uniform results.
+// with the BM tokens in LDS (token t at xs[t * NU * 64], a compile-time
+// stride, so that the tokens of a unit are read with immediate offsets from
+// one address); wave-uniform results.
 // Units past the row's end (u >= U) hold a repeat of its last unit and are
 // left out with a select, not a branch.
 template <int BM, int NU>
@@ -125,7 +127,7 @@ __device__ inline void row_dots(const u32x4 (&v)[NU], const u32x4* xs, int U, in
     const int uc = min(u, U - 1);
 #pragma unroll
     for (int t = 0; t < BM; ++t) {
-      const float s = dot8(v[j], xs[t * U + uc], acc[t]);
+      const float s = dot8(v[j], xs[t * (NU * kWave) + uc], acc[t]);
       acc[t] = u < U ? s : acc[t];
     }
   }

@@ -63,10 +63,20 @@ extern "C" hipError_t si_trace_wave_read(void* dst, size_t bytes) {
 constexpr int kMaxOwnRows = 256;                   // rows one block owns (at most)
 constexpr int kMaxOwnSub = kMaxOwnRows / kWave;    // 64-row passes of one block (4)
 constexpr int kCountWord = 4 * kMaxOwnSub;         // published word that holds the block's kept count
-constexpr int kMaxPairs = kWave;                   // (owner block, pass) pairs of one down chunk
-constexpr int kMaxChunkRows = 4096;                // rows of one down chunk (at most)
-constexpr int kFin = kLWaves - 1;                  // the wave that finishes the prediction
+constexpr int kMaxPairs = kWave;                   // (owner block, pass) pairs of one group
+constexpr int kMaxChunkRows = 4096;                // kept rows of one group (at most)
 static_assert(kCountWord < kOwnPubStride, "published words of a block");
+
+// Eight wavefronts per block (two per SIMD), so that a wave may hold up to
+// 256 registers: a row of W_gate and of W_up in flight together, and the
+// accumulators of 8 tokens, without spilling.
+constexpr int kOW = 8;
+constexpr int kOT = kOW * kWave;
+constexpr int kOSignUnits = (kMaxD / 128 + kOW - 1) / kOW;  // sign units per wave and pass, at most (8)
+constexpr int kFin = kOW - 1;      // the wave that finishes the prediction
+constexpr int kODN = 8;            // W_down^T pieces per wave and down round
+constexpr int kODownRound = kOW * kODN;
+static_assert(kODN * kMaxB <= kWave, "a wave polls the h3 words of its pieces, one lane per (piece, token)");
 
 struct OwnedArgs {
   const u32x4* signs;
@@ -94,29 +104,23 @@ struct OwnedArgs {
 template <int BM, int NU>
 struct OwnedLds {
   static constexpr int kUnits = NU * kWave;
-  static constexpr int kFold = kLWaves / BM;
+  static constexpr int kFold = kOW / BM;  // per-wave partial tiles held at once in the fold
   // tokens (fp16); once the gate/up work is done, the per-wave partial tiles
   union {
     u32x4 xs[BM * kUnits];
     float dpart[kFold][BM][kTile];
   };
   uint32_t xw[BM * kUnits / 4];  // sign words of the tokens
-  // per-wave N_neg partial counts during the prediction; the down chunk's
-  // masks, their prefix and its ordered kept rows afterwards
+  // per-wave N_neg partial counts during the prediction; the group's kept
+  // rows in order afterwards
   union {
-    int cpart[kLWaves][BM][kWave];
-    struct {
-      uint32_t pm[4 * kMaxPairs];
-      uint32_t dent[kMaxChunkRows];  // conf << 31 | row
-    } ch;
+    int cpart[kOW][BM][kWave];
+    uint32_t dent[kMaxChunkRows];  // conf << 31 | row
   };
-  float dots[kRoundRows][2][BM];
-  float h1[kRoundRows][BM];
-  uint32_t need[kRoundRows];
+  uint32_t pm[4 * kMaxPairs];  // the group's published mask words
   uint32_t srow[kMaxOwnRows];  // conf << 31 | row of the block's kept rows, ascending
-  float hs[kDownRound * BM];   // h3 of the down round's positions
-  int wsum[kLWaves];
-  int n_own, n_late, n_up, n_down, zok;
+  int wsum[kOW];
+  int n_own, n_up, n_down;
   uint32_t epoch;
 };
 
@@ -167,14 +171,60 @@ __device__ inline int block_sum(OwnedLds<BM, NU>& L, int v, int lane, int wv) {
   v = wave_sum_int(v);
   if (lane == 0) L.wsum[wv] = v;
   __syncthreads();
-  int t = lane < kLWaves ? L.wsum[lane] : 0;
+  int t = lane < kOW ? L.wsum[lane] : 0;
   t = wave_sum_int(t);
   __syncthreads();
   return t;
 }
 
+// Sum of every block's published kept count (one poll per thread of the
+// calling threads [t0, t0 + nt)); proof too that every block has read the
+// call counter.
+__device__ inline int census_part(const uint64_t* pub, int P, int t, int nt, uint32_t tag, uint32_t* hdr) {
+  int sum = 0;
+  for (int o = t; o < P; o += nt) {
+    const uint64_t* src[1] = {&pub[(size_t)o * kOwnPubStride + kCountWord]};
+    uint32_t v[1];
+    poll_words<1>(src, 1, tag, hdr, v);
+    sum += (int)v[0];
+  }
+  return sum;
+}
+
+// Dot products of two rows held as NU 16-byte units per lane (unit lane +
+// 64 j) with the BM tokens in LDS (token t at xs[t * NU * 64]); each token
+// unit is read once for both rows.  Wave-uniform results.
 template <int BM, int NU>
-__global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
+__device__ inline void row_dots2(const u32x4 (&v)[NU], const u32x4 (&w)[NU], const u32x4* xs, int U, int lane,
+                                 float (&o1)[BM], float (&o2)[BM]) {
+  float a1[BM], a2[BM];
+#pragma unroll
+  for (int t = 0; t < BM; ++t) a1[t] = a2[t] = 0.f;
+#pragma unroll
+  for (int j = 0; j < NU; ++j) {
+    const int u = lane + kWave * j;
+    const int uc = min(u, U - 1);
+#pragma unroll
+    for (int t = 0; t < BM; ++t) {
+      const u32x4 xv = xs[t * (NU * kWave) + uc];
+      const float s1 = dot8(v[j], xv, a1[t]);
+      const float s2 = dot8(w[j], xv, a2[t]);
+      a1[t] = u < U ? s1 : a1[t];
+      a2[t] = u < U ? s2 : a2[t];
+    }
+    // one unit's token values live at a time (with 8 tokens the scheduler
+    // would otherwise hoist every unit's LDS reads and spill)
+    if constexpr (BM >= 4) __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int t = 0; t < BM; ++t) {
+    o1[t] = wave_total(a1[t]);
+    o2[t] = wave_total(a2[t]);
+  }
+}
+
+template <int BM, int NU>
+__global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
   OwnedLds<BM, NU>& L = *reinterpret_cast<OwnedLds<BM, NU>*>(lds_raw);
 
@@ -197,14 +247,20 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
   // the wait for it, which comes at once for an atomic load, also covers
   // them) the call counter; addresses are clamped so that the requests are
   // unconditional and go out back to back; tokens b..BM-1 are zero
-  u32x4 sreg[kMaxSignUnitsPerWave];
+  // a row has d/128 <= 4 NU sign units, so a wave counts at most
+  // ceil(NU / 2) of them per pass; the requests are unconditional (clamped
+  // unit, the same line again where a wave has fewer) so that the counts
+  // can start as the first ones arrive
+  constexpr int kSU = (NU + 1) / 2;
+  static_assert(kSU <= kOSignUnits, "sign units per wave");
+  u32x4 sreg[kSU];
   const int kpad = (k + kRowGroup - 1) / kRowGroup * kRowGroup;  // rows of the packed layout
   auto load_signs = [&](int s) {
     const u32x4* sg = a.signs + r0 + min(s * kWave + lane, Rb - 1);
 #pragma unroll
-    for (int i = 0; i < kMaxSignUnitsPerWave; ++i) {
-      const int q = wv + kLWaves * i;
-      if (q < units) sreg[i] = load_nt(sg + (size_t)q * kpad);
+    for (int i = 0; i < kSU; ++i) {
+      const int q = min(wv + kOW * i, units - 1);
+      sreg[i] = load_nt(sg + (size_t)q * kpad);
     }
   };
   uint32_t mbyte = 0;
@@ -222,19 +278,20 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
     }
   }
   {
+    // token t's unit u at xs[t * XS + u] (XS = NU * 64 >= U)
+    constexpr int XS = OwnedLds<BM, NU>::kUnits;
     const u32x4* xg = reinterpret_cast<const u32x4*>(a.x);
     const int nx = b * U;
-    for (int i = tid; i < BM * U; i += kLThreads) {
-      const u32x4 xv = xg[min(i, nx - 1)];
+    for (int i = tid; i < BM * XS; i += kOT) {
+      const int t = i / XS, u = i - t * XS;
+      const u32x4 xv = xg[min(t * U + u, nx - 1)];
       if (i == tid && tid == 0) {
         asm volatile("" ::: "memory");
         L.epoch = ld_agent(&a.hdr[H_EPOCH]);
         L.n_up = 0;
         L.n_down = 0;
-        L.zok = 0;
-        L.n_late = 0;
       }
-      L.xs[i] = i < nx ? xv : u32x4{0, 0, 0, 0};
+      L.xs[i] = (t < b && u < U) ? xv : u32x4{0, 0, 0, 0};
     }
   }
   __syncthreads();
@@ -245,18 +302,17 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
   // for every outstanding request, stores included, inside it)
   bool mkeep = mbyte != 0;
   if (predict) {
-    for (int i = tid; i < b * W; i += kLThreads) {
+    for (int i = tid; i < BM * W; i += kOT) {  // tokens b..BM-1 are zero
       const int t = i / W, w = i - t * W;
-      L.xw[i] = sign_word(&L.xs[t * U + 4 * w]);
+      L.xw[i] = sign_word(&L.xs[t * OwnedLds<BM, NU>::kUnits + 4 * w]);
     }
   }
   __syncthreads();
   SI_TRACE_MARK(1);
 
   // ---- 1. kept and confident masks of the owned rows, 64 rows per pass;
-  // the finishing wave (the last one, which almost never has gate/up work in
-  // the first round) applies the rule, lists the kept rows in order and
-  // publishes, so no other wave waits for those stores
+  // the finishing wave applies the rule, lists the kept rows in order and
+  // publishes, so no wave with gate/up work waits for those stores
   int n_own = 0;  // finishing wave
   for (int s = 0; s < nsub; ++s) {
     const bool any_rows = s * kWave < Rb;
@@ -265,46 +321,42 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
       int c[BM];
 #pragma unroll
       for (int t = 0; t < BM; ++t) c[t] = 0;
-      bool any_unit = false;
 #pragma unroll
-      for (int i = 0; i < kMaxSignUnitsPerWave; ++i) {
-        const int q = wv + kLWaves * i;
-        if (q < units) {
-          any_unit = true;
+      for (int i = 0; i < kSU; ++i) {
+        const int q = wv + kOW * i;
+        const int qc = min(q, units - 1);
 #pragma unroll
-          for (int t = 0; t < BM; ++t) {
-            if (t < b) {
-              const u32x4 xv = *reinterpret_cast<const u32x4*>(&L.xw[t * W + 4 * q]);
-              c[t] += __popc(sreg[i].x ^ xv.x) + __popc(sreg[i].y ^ xv.y) + __popc(sreg[i].z ^ xv.z) +
-                      __popc(sreg[i].w ^ xv.w);
-            }
-          }
+        for (int t = 0; t < BM; ++t) {
+          const u32x4 xv = *reinterpret_cast<const u32x4*>(&L.xw[t * W + 4 * qc]);
+          const int n = __popc(sreg[i].x ^ xv.x) + __popc(sreg[i].y ^ xv.y) + __popc(sreg[i].z ^ xv.z) +
+                        __popc(sreg[i].w ^ xv.w);
+          c[t] += q < units ? n : 0;
         }
       }
-      if (any_unit) {
+      // every wave stores its partial counts (zero without units)
 #pragma unroll
-        for (int t = 0; t < BM; ++t)
-          if (t < b) L.cpart[wv][t][lane] = c[t];
-      }
+      for (int t = 0; t < BM; ++t) L.cpart[wv][t][lane] = c[t];
       __syncthreads();
       if (s == 0) SI_TRACE_MARK(2);
     }
     if (wv == kFin) {
+      // every request of this wave has completed here (the sign units for
+      // the counts, the tile's zeroing stores before the tokens); said
+      // explicitly so that the publishing stores below are not waited for
+      wait_all_requests();
       const int i = s * kWave + lane;
       const int row = r0 + i;
       const bool valid = i < Rb;
       bool keep = false, conf = false;
       if (predict) {
         if (any_rows) {
-          const int nw = min(units, kLWaves);  // waves that counted units
 #pragma unroll
           for (int t = 0; t < BM; ++t) {
-            if (t < b) {
-              int n_neg = 0;
-              for (int w = 0; w < nw; ++w) n_neg += L.cpart[w][t][lane];
-              keep |= n_neg < a.T;
-              conf |= n_neg < a.T - a.margin;
-            }
+            int n_neg = 0;
+#pragma unroll
+            for (int w = 0; w < kOW; ++w) n_neg += L.cpart[w][t][lane];
+            keep |= t < b && n_neg < a.T;
+            conf |= t < b && n_neg < a.T - a.margin;
           }
         }
       } else if (any_rows) {
@@ -313,33 +365,29 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
         conf = keep;
       }
       keep = keep && valid;
-      if (s == 0) SI_TRACE_WAVE(5);
       const uint64_t kb = __ballot(keep);
       const uint64_t cb = __ballot(keep && conf);
       if (keep) L.srow[n_own + __popcll(kb & lanes_below(lane))] = (uint32_t)row | (conf ? 0x80000000u : 0u);
       n_own += __popcll(kb);
-      if (lane < 4) {
+      // lanes 0-3: this pass's kept and confident words; after the last
+      // pass lane 4 also publishes the block's kept count (in the same
+      // store instruction, before any later request of this wave)
+      const bool last = s + 1 == nsub;
+      if (lane < 4 || (last && lane == 4)) {
         const uint64_t m = lane < 2 ? kb : cb;
-        st_agent64(&a.pub[(size_t)blk * kOwnPubStride + 4 * s + lane],
-                   tagged(tag, (uint32_t)(m >> (32 * (lane & 1)))));
+        const uint32_t v = lane < 4 ? (uint32_t)(m >> (32 * (lane & 1))) : (uint32_t)n_own;
+        st_agent64(&a.pub[(size_t)blk * kOwnPubStride + (lane < 4 ? 4 * s + lane : kCountWord)], tagged(tag, v));
       }
       if (valid && a.mask) a.mask[row] = keep ? 1 : 0;
-      if (s == 0) SI_TRACE_WAVE(6);
+      if (last && lane == 0) L.n_own = n_own;
     }
     if (predict && any_rows && s + 1 < nsub) __syncthreads();  // the partial counts are reused
   }
-  if (wv == kFin) {
-    SI_TRACE_MARK(4);
-    if (lane == 0) {
-      L.n_own = n_own;
-      st_agent64(&a.pub[(size_t)blk * kOwnPubStride + kCountWord], tagged(tag, (uint32_t)n_own));
-    }
-  }
-  if (wv == kFin) SI_TRACE_WAVE(7);
   __syncthreads();
   n_own = uniform(L.n_own);
   SI_TRACE_MARK(3);
 
+  bool census_done = false;
   if (a.mlp) {
     // ---- the block's group: the T blocks [g T, g T + T) (T = tiles of y);
     // member m takes an even share of the group's kept rows for gate/up and
@@ -352,15 +400,28 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
     // the group's mask words, one per thread (waves 0..3), before any
     // gate/up request is out (a round trip behind the grid's row requests
     // would take several times as long)
+    // block 0's waves 4..7 meanwhile take the census: every block's kept
+    // count (the call's count, and proof that every block has read the call
+    // counter, which block 0 then advances)
     if (tid < 4 * npairs) {
       const int p = tid >> 2;
       const int o = g * T + p / nsub, sb = p - (p / nsub) * nsub;
       const uint64_t* src[1] = {&a.pub[(size_t)o * kOwnPubStride + 4 * sb + (tid & 3)]};
       uint32_t v[1];
       poll_words<1>(src, 1, tag, a.hdr, v);
-      L.ch.pm[tid] = v[0];
+      L.pm[tid] = v[0];
+    } else if (blk == 0 && tid >= kOT / 2) {
+      const int sum = wave_sum_int(census_part(a.pub, P, tid - kOT / 2, kOT / 2, tag, a.hdr));
+      if (lane == 0) L.wsum[wv] = sum;
     }
     __syncthreads();
+    if (blk == 0 && tid == 0) {
+      int sum = 0;
+      for (int w = kOW / 2; w < kOW; ++w) sum += L.wsum[w];
+      if (a.n_out) *a.n_out = sum;
+      advance_epoch(a.hdr, epoch);
+    }
+    census_done = true;
     if (owns_tile && wv == kFin) {  // the tile's zeroing stores have landed by now
       wait_own_stores();
       if (lane == 0) st_agent64(&a.zflag[blk], tagged(tag, 1u));
@@ -368,19 +429,19 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
     // the group's kept rows in order: every wave forms the prefix of the
     // pairs' kept counts (lane = pair), then one wave per pair writes its
     // rows' entries (lane = row)
-    const int cnt = lane < npairs ? __popc(L.ch.pm[4 * lane]) + __popc(L.ch.pm[4 * lane + 1]) : 0;
+    const int cnt = lane < npairs ? __popc(L.pm[4 * lane]) + __popc(L.pm[4 * lane + 1]) : 0;
     const int incl = wave_incl_scan(cnt);
     const int pre = incl - cnt;
     const int n = min(uniform(__builtin_amdgcn_readlane(incl, kWave - 1)), kMaxChunkRows);
-    for (int p = wv; p < npairs; p += kLWaves) {
-      const uint64_t kb = (uint64_t)L.ch.pm[4 * p] | ((uint64_t)L.ch.pm[4 * p + 1] << 32);
-      const uint64_t cb = (uint64_t)L.ch.pm[4 * p + 2] | ((uint64_t)L.ch.pm[4 * p + 3] << 32);
+    for (int p = wv; p < npairs; p += kOW) {
+      const uint64_t kb = (uint64_t)L.pm[4 * p] | ((uint64_t)L.pm[4 * p + 1] << 32);
+      const uint64_t cb = (uint64_t)L.pm[4 * p + 2] | ((uint64_t)L.pm[4 * p + 3] << 32);
       const int q0p = __builtin_amdgcn_readlane(pre, p);
       if ((kb >> lane) & 1ull) {
         const int o = g * T + p / nsub, sb = p - (p / nsub) * nsub;
         const uint32_t row = (uint32_t)(o * R + sb * kWave + lane);
         const int q = q0p + __popcll(kb & lanes_below(lane));
-        if (q < kMaxChunkRows) L.ch.dent[q] = row | (((cb >> lane) & 1ull) ? 0x80000000u : 0u);
+        if (q < kMaxChunkRows) L.dent[q] = row | (((cb >> lane) & 1ull) ? 0x80000000u : 0u);
       }
     }
     const int lo = (n * m) / T, hi = (n * (m + 1)) / T;  // this member's gate/up positions
@@ -388,180 +449,110 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
     __syncthreads();
     SI_TRACE_MARK(4);
 
-    // down requests of a round: this wave's positions q0 + wv + 16 j
-    u32x4 vd[kDN];
-    uint32_t dloaded = 0;
-    const int dunit = tile * kWave + lane;
-    const bool dcol_ok = dunit < U;
-    auto issue_down = [&](int q0) {
-      dloaded = 0;
-#pragma unroll
-      for (int j = 0; j < kDN; ++j) {
-        vd[j] = u32x4{0, 0, 0, 0};
-        const int q = q0 + wv + kLWaves * j;
-        if (q < dN) {
-          const uint32_t e = L.ch.dent[q];
-          if ((spec_ok && (e >> 31)) || no_as) {
-            if (dcol_ok) vd[j] = load_nt(a.wdt + (size_t)(e & 0x7fffffffu) * U + dunit);
-            dloaded |= 1u << j;
-          }
-        }
-      }
-    };
-
-    // ---- 2. gate/up over the member's positions [lo, hi) of the group's
-    // list (the first round runs also when there are none)
-    const int ir = wv >> 1, imat = wv & 1;
-    for (int r0r = lo, first = 1;; r0r += kRoundRows, first = 0) {
-      const int mr = max(0, min(kRoundRows, hi - r0r));
-      const uint32_t* srow = &L.ch.dent[r0r];
-      if (!first) __syncthreads();
-      const uint32_t e = ir < mr ? srow[ir] : kBadRow;
-      // the row's requests and their use sit in one branch, so that no
-      // request is left outstanding across rounds (the compiler then issues
-      // them back to back instead of waiting before each)
-      if (e != kBadRow && (imat == 0 || (spec_ok && (e >> 31)))) {
-        u32x4 v[NU];
-        load_row<NU>((imat ? a.wu : a.wg) + (size_t)(e & 0x7fffffffu) * U, U, lane, v);
+    // ---- 2. gate/up: wave w takes positions lo + w, lo + w + 8, ... and
+    // for each its W_gate row and (for confident rows, or without actual
+    // sparsity) its W_up row at once; other rows read W_up only where some
+    // token's ReLU output is positive.  Each wave works through its rows on
+    // its own (no block barrier) and publishes h3 per row and token.
+    int n_up = 0;
+    for (int pos = lo + wv; pos < hi; pos += kOW) {
+      const uint32_t e = L.dent[pos];
+      const uint32_t row = e & 0x7fffffffu;
+      float g[BM], u[BM];
+      bool up;
+      // a row's requests and their use sit in one branch (row-uniform)
+      if ((spec_ok && (e >> 31)) || no_as) {
+        u32x4 vg[NU], vu[NU];
+        load_row<NU>(a.wg + (size_t)row * U, U, lane, vg);
+        load_row<NU>(a.wu + (size_t)row * U, U, lane, vu);
         SI_TRACE_WAVE(0);
-        float dt[BM];
-        row_dots<BM, NU>(v, L.xs, U, lane, dt);
-        if (lane == 0) {
+        row_dots2<BM, NU>(vg, vu, L.xs, U, lane, g, u);
+        up = true;
+      } else {
+        u32x4 vg[NU];
+        load_row<NU>(a.wg + (size_t)row * U, U, lane, vg);
+        row_dots<BM, NU>(vg, L.xs, U, lane, g);
+        bool any = false;
 #pragma unroll
-          for (int t = 0; t < BM; ++t) L.dots[ir][imat][t] = dt[t];
-        }
-      }
-      SI_TRACE_WAVE(1);
-      // the item's W_down^T pieces go out once this wave's gate/up data is
-      // in, so they stream behind the loads that h3 depends on (issued
-      // before them, they would only delay h3: the requests of a wave
-      // complete in order)
-      if (first) issue_down(0);
-      __syncthreads();
-      if (wv == 0 && mr > 0) {  // rows of the round: one per lane (mr <= 8)
-        bool any = no_as, spec = false;
-        if (lane < mr) {
+        for (int t = 0; t < BM; ++t) any |= g[t] > 0.f;
+        up = any;
+        if (any) {
+          u32x4 vu[NU];
+          load_row<NU>(a.wu + (size_t)row * U, U, lane, vu);
+          row_dots<BM, NU>(vu, L.xs, U, lane, u);
+        } else {
 #pragma unroll
-          for (int t = 0; t < BM; ++t) {
-            const float h = fmaxf(L.dots[lane][0][t], 0.f);
-            L.h1[lane][t] = h;
-            any |= h > 0.f;
-          }
-          spec = spec_ok && (srow[lane] >> 31);
-          L.need[lane] = (any && !spec) ? 1u : 0u;
-        }
-        const uint64_t late = __ballot(lane < mr && any && !spec);
-        const uint64_t upr = __ballot(lane < mr && (any || spec));
-        if (lane == 0) {
-          L.n_late = __popcll(late);
-          L.n_up += __popcll(upr);
+          for (int t = 0; t < BM; ++t) u[t] = 0.f;
         }
       }
-      __syncthreads();
-      if (mr > 0 && L.n_late) {  // W_up rows whose gate value asks for them
-        if (imat == 1 && ir < mr && L.need[ir]) {
-          u32x4 v[NU];
-          load_row<NU>(a.wu + (size_t)(srow[ir] & 0x7fffffffu) * U, U, lane, v);
-          float dt[BM];
-          row_dots<BM, NU>(v, L.xs, U, lane, dt);
-          if (lane == 0) {
+      n_up += up ? 1 : 0;
+      float hv = 0.f;  // lane t holds token t's h3
 #pragma unroll
-            for (int t = 0; t < BM; ++t) L.dots[ir][1][t] = dt[t];
-          }
-        }
-        __syncthreads();
-      }
-      for (int i = tid; i < mr * BM; i += kLThreads) {
-        const int r = i / BM, t = i - r * BM;
-        if (t < b) {
-          const bool spec = spec_ok && (srow[r] >> 31);
-          const float h = (L.need[r] || spec) ? L.h1[r][t] * L.dots[r][1][t] : 0.f;
-          st_agent64(&a.h3e[(size_t)(srow[r] & 0x7fffffffu) * b + t], tagged(tag, __float_as_uint(h)));
-        }
-      }
-      if (r0r + kRoundRows >= hi) break;
+      for (int t = 0; t < BM; ++t) hv = lane == t ? fmaxf(g[t], 0.f) * u[t] : hv;
+      if (lane < b) st_agent64(&a.h3e[(size_t)row * b + lane], tagged(tag, __float_as_uint(hv)));
     }
+    SI_TRACE_WAVE(1);
+    if (lane == 0 && n_up) atomicAdd(&L.n_up, n_up);
     SI_TRACE_MARK(6);
 
-    // ---- 3. down-projection of (tile, chunk)
+    // ---- 3. down-projection of (tile, the group's rows): per round, wave w
+    // takes positions q0 + w + 8 j (j < 8); it requests the tile's W_down^T
+    // pieces of the confident ones, then polls their h3 words (lane = piece
+    // x token; in the first round wave 0's last lane polls the tile's zero
+    // flag in the same requests), fetches the non-confident pieces whose h3
+    // is non-zero, and accumulates
     float acc[BM][8];
 #pragma unroll
     for (int t = 0; t < BM; ++t)
 #pragma unroll
       for (int q = 0; q < 8; ++q) acc[t][q] = 0.f;
     int n_down = 0;
-    bool census_done = false;
-    for (int q0 = 0; q0 < dN; q0 += kDownRound) {
-      const int nq = min(kDownRound, dN - q0);
-      if (q0 != 0) {
-        __syncthreads();  // the previous round's h3 values have been used
-        issue_down(q0);
-      }
-      // waves 0..3 collect the round's h3 words (slot = position x BM +
-      // token, all requests in flight together); in the first round wave 4
-      // checks the tile's zero flag and waves 8.. of block 0 take the census
-      if (tid < kDownPollThreads) {
-        constexpr int kPer = (kDownRound * BM + kDownPollThreads - 1) / kDownPollThreads;
-        const uint64_t* src[kPer];
-        int nv = 0;
+    bool zok = false;
+    const int dunit = tile * kWave + lane;
+    const bool dcol_ok = dunit < U;
+    constexpr bool kZLane = kODN * BM < kWave;  // wave 0's lane 63 is free for the zero flag
+    for (int q0 = 0; q0 < dN; q0 += kODownRound) {
+      u32x4 vd[kODN];
+      uint32_t dl = 0;
 #pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-          const int j = tid + kDownPollThreads * i;
-          const int q = j / BM, t = j - q * BM;
-          const bool ok = q < nq && t < b;
-          const int qc = ok ? q : 0;
-          src[i] = a.h3e + (size_t)(L.ch.dent[q0 + qc] & 0x7fffffffu) * b + (ok ? t : 0);
-          if (ok) nv = i + 1;  // slots of one thread are valid as a prefix
+      for (int j = 0; j < kODN; ++j) {
+        vd[j] = u32x4{0, 0, 0, 0};
+        const int q = q0 + wv + kOW * j;
+        if (q < dN) {
+          const uint32_t e = L.dent[q];
+          if ((spec_ok && (e >> 31)) || no_as) {
+            if (dcol_ok) vd[j] = load_nt(a.wdt + (size_t)(e & 0x7fffffffu) * U + dunit);
+            dl |= 1u << j;
+          }
         }
-        uint32_t hv[kPer];
-        poll_words<kPer>(src, nv, tag, a.hdr, hv);
-#pragma unroll
-        for (int i = 0; i < kPer; ++i) {
-          const int j = tid + kDownPollThreads * i;
-          if (j < kDownRound * BM) L.hs[j] = i < nv ? __uint_as_float(hv[i]) : 0.f;
-        }
-      } else if (q0 == 0 && wv == kDownPollThreads / kWave) {
-        bool abort = false;
-        poll_lane(&a.zflag[tile], lane == 0, tag, a.hdr, abort);
-        if (lane == 0 && !abort) L.zok = 1;
-      } else if (q0 == 0 && blk == 0 && wv >= kLWaves / 2) {
-        // every block's kept count: the call's count, and proof that every
-        // block has read the call counter
-        int sum = 0;
-        for (int o = tid - kLThreads / 2; o < P; o += kLThreads / 2) {
-          const uint64_t* src[1] = {&a.pub[(size_t)o * kOwnPubStride + kCountWord]};
-          uint32_t v[1];
-          poll_words<1>(src, 1, tag, a.hdr, v);
-          sum += (int)v[0];
-        }
-        sum = wave_sum_int(sum);
-        if (lane == 0) L.wsum[wv] = sum;
       }
-      __syncthreads();
-      if (q0 == 0 && blk == 0) {
-        if (tid == 0) {
-          int n = 0;
-          for (int w = kLWaves / 2; w < kLWaves; ++w) n += L.wsum[w];
-          if (a.n_out) *a.n_out = n;
-          advance_epoch(a.hdr, epoch);
-        }
-        census_done = true;
-      }
+      // h3 of (piece j, token t) in lane j * BM + t
+      const int pj = lane / BM, pt = lane - pj * BM;
+      const int pq = q0 + wv + kOW * pj;
+      const bool pok = pj < kODN && pq < dN && pt < b;
+      const bool zlane = kZLane && q0 == 0 && wv == 0 && lane == kWave - 1;
+      const uint64_t* src[1] = {zlane ? &a.zflag[tile]
+                                      : a.h3e + (size_t)(L.dent[pok ? pq : q0] & 0x7fffffffu) * b + (pok ? pt : 0)};
+      uint32_t hw[1];
+      poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
+      if (q0 == 0 && wv == 0) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
       if (q0 == 0) SI_TRACE_WAVE(3);
 #pragma unroll
-      for (int j = 0; j < kDN; ++j) {
-        const int q = wv + kLWaves * j;
+      for (int j = 0; j < kODN; ++j) {
+        const int q = q0 + wv + kOW * j;
         float hv[BM];
         bool nz = false;
 #pragma unroll
         for (int t = 0; t < BM; ++t) {
-          hv[t] = (q < nq && t < b) ? L.hs[q * BM + t] : 0.f;
+          hv[t] = (j * BM + t < kWave && q < dN && t < b)
+                      ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(hw[0], min(j * BM + t, kWave - 1)))
+                      : 0.f;
           nz |= hv[t] != 0.f;
         }
-        if (q < nq && !((dloaded >> j) & 1u) && nz) {  // late request
-          const uint32_t e = L.ch.dent[q0 + q];
+        if (q < dN && !((dl >> j) & 1u) && nz) {  // late request
+          const uint32_t e = L.dent[q];
           if (dcol_ok) vd[j] = load_nt(a.wdt + (size_t)(e & 0x7fffffffu) * U + dunit);
-          dloaded |= 1u << j;
+          dl |= 1u << j;
         }
         const f16x2 p0 = as_h2(vd[j].x), p1 = as_h2(vd[j].y), p2 = as_h2(vd[j].z), p3 = as_h2(vd[j].w);
         const float f[8] = {(float)p0.x, (float)p0.y, (float)p1.x, (float)p1.y,
@@ -571,35 +562,37 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
 #pragma unroll
           for (int qq = 0; qq < 8; ++qq) acc[t][qq] = fmaf(hv[t], f[qq], acc[t][qq]);
       }
-      n_down += __popc(dloaded);
+      n_down += __popc(dl);
       if (q0 == 0) SI_TRACE_WAVE(4);
     }
+    if (lane == 0 && tile == 0 && n_down) atomicAdd(&L.n_down, n_down);
+    if (wv == 0 && lane == 0) L.wsum[0] = zok ? 1 : 0;
     // per-wave partial tiles folded in LDS (plain stores; x is no longer
     // needed): kFold waves store, the others add in turn
     constexpr int kFold = OwnedLds<BM, NU>::kFold;
+    __syncthreads();
+    const bool zok_all = L.wsum[0] != 0;
     if (dN > 0) {
 #pragma unroll
-      for (int pass = 0; pass < kLWaves / kFold; ++pass) {
+      for (int pass = 0; pass < kOW / kFold; ++pass) {
         if (wv / kFold == pass) {
-          const int s = wv - pass * kFold;
+          const int s2 = wv - pass * kFold;
 #pragma unroll
           for (int t = 0; t < BM; ++t)
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
-              float& dst = L.dpart[s][t][lane * 8 + q];
+              float& dst = L.dpart[s2][t][lane * 8 + q];
               dst = pass == 0 ? acc[t][q] : dst + acc[t][q];
             }
         }
-        if (pass + 1 < kLWaves / kFold) __syncthreads();
+        __syncthreads();
       }
     }
-    if (lane == 0 && tile == 0 && n_down) atomicAdd(&L.n_down, n_down);
     SI_TRACE_MARK(8);
-    __syncthreads();
 
     // ---- the item's tile into y (its owner zeroed it in this call)
     if (dN > 0) {
-      if (tid == 0 && !L.zok) {  // only after a timed-out poll
+      if (tid == 0 && !zok_all) {  // after a timed-out poll, or when no lane was free for it
         long spins = 0;
         while ((uint32_t)(ld_agent64(&a.zflag[tile]) >> 32) != tag) {
           if (++spins > kPollLimit) {
@@ -611,41 +604,21 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
       }
       __syncthreads();
       SI_TRACE_MARK(9);
-      for (int i = tid; i < b * kTile; i += kLThreads) {
+      for (int i = tid; i < b * kTile; i += kOT) {
         const int t = i / kTile, c = i - t * kTile, col = tile * kTile + c;
         float v = 0.f;
 #pragma unroll
-        for (int s = 0; s < kFold; ++s) v += L.dpart[s][t][c];
+        for (int s2 = 0; s2 < kFold; ++s2) v += L.dpart[s2][t][c];
         if (col < d && v != 0.f) unsafeAtomicAdd(&a.y[(size_t)t * d + col], v);
-      }
-    }
-    if (blk == 0 && !census_done) {
-      int sum = 0;
-      for (int o = tid; o < P; o += kLThreads) {
-        const uint64_t* src[1] = {&a.pub[(size_t)o * kOwnPubStride + kCountWord]};
-        uint32_t v[1];
-        poll_words<1>(src, 1, tag, a.hdr, v);
-        sum += (int)v[0];
-      }
-      sum = block_sum(L, sum, lane, wv);
-      if (tid == 0) {
-        if (a.n_out) *a.n_out = sum;
-        advance_epoch(a.hdr, epoch);
       }
     }
     if (tid == 0) {
       a.counts[2 * blk] = L.n_up;
       a.counts[2 * blk + 1] = L.n_down;
     }
-  } else if (blk == 0) {  // the predictor alone: the census of block 0
-    int sum = 0;
-    for (int o = tid; o < P; o += kLThreads) {
-      const uint64_t* src[1] = {&a.pub[(size_t)o * kOwnPubStride + kCountWord]};
-      uint32_t v[1];
-      poll_words<1>(src, 1, tag, a.hdr, v);
-      sum += (int)v[0];
-    }
-    sum = block_sum(L, sum, lane, wv);
+  }
+  if (blk == 0 && !census_done) {  // the predictor alone: the census of block 0
+    const int sum = block_sum(L, census_part(a.pub, P, tid, kOT, tag, a.hdr), lane, wv);
     if (tid == 0) {
       if (a.n_out) *a.n_out = sum;
       advance_epoch(a.hdr, epoch);
@@ -655,14 +628,14 @@ __global__ __launch_bounds__(kLThreads) void k_owned(OwnedArgs a) {
   // ---- the ascending kept list: the counts of the blocks before this one
   if (a.idx) {
     int sum = 0;
-    for (int o = tid; o < blk; o += kLThreads) {
+    for (int o = tid; o < blk; o += kOT) {
       const uint64_t* src[1] = {&a.pub[(size_t)o * kOwnPubStride + kCountWord]};
       uint32_t v[1];
       poll_words<1>(src, 1, tag, a.hdr, v);
       sum += (int)v[0];
     }
     const int before = block_sum(L, sum, lane, wv);
-    for (int q = tid; q < n_own; q += kLThreads) a.idx[before + q] = (int32_t)(L.srow[q] & 0x7fffffffu);
+    for (int q = tid; q < n_own; q += kOT) a.idx[before + q] = (int32_t)(L.srow[q] & 0x7fffffffu);
   }
   SI_TRACE_MARK(10);
   SI_TRACE_FLUSH;
@@ -689,7 +662,7 @@ static int owned_blocks() {
       if (hipGetDevice(&dev) != hipSuccess) return 0;
       if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
       if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return 0;
-      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kLThreads, lds) != hipSuccess) return 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kOT, lds) != hipSuccess) return 0;
       if (per_cu >= 1) blocks = cus < kMaxLayerBlocks ? cus : kMaxLayerBlocks;
     }
   }
@@ -733,7 +706,7 @@ static hipError_t owned_b(const LayerCall& c, hipStream_t s) {
     a.zflag = reinterpret_cast<uint64_t*>(base + L.zflag);
     a.counts = reinterpret_cast<int32_t*>(base + L.counts);
     a.y = c.y;
-    k_owned<BM, NU><<<P, kLThreads, owned_lds_bytes<BM, NU>(), s>>>(a);
+    k_owned<BM, NU><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !c.counters || !c.y) return e;
     return launch_sum_counts(a.counts, P, c.n_out, k, c.counters, s);

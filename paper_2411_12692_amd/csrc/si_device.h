@@ -126,6 +126,13 @@ __device__ inline uint32_t epoch_tag(uint32_t epoch) { return (epoch & 0x7ffffff
 // announces.  (Consumers also check every word's tag.)
 __device__ inline void wait_own_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Wait for every outstanding vector memory request of the wave, as an
+// instruction the compiler's wait-count pass sees (inline assembly is opaque
+// to it): afterwards it knows that no load is pending, so it inserts no
+// blanket wait, which would also wait for stores issued later, where a
+// register of a possibly pending load is reused.
+__device__ inline void wait_all_requests() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 __device__ inline uint32_t ld_agent(const uint32_t* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -215,20 +222,26 @@ constexpr int kTraceWaveMarks = 8;
 #ifdef SI_TRACE
 extern __device__ uint64_t g_si_trace[];
 extern __device__ uint64_t g_si_trace_wave[];
-#define SI_TRACE_DECL                          \
-  uint64_t si_tr_[kTraceBlockMarks] = {};      \
-  uint64_t si_trw_[kTraceWaveMarks] = {}
-#define SI_TRACE_MARK(slot) (si_tr_[(slot)] = __builtin_amdgcn_s_memrealtime())
-#define SI_TRACE_WAVE(mark) (si_trw_[(mark)] = __builtin_amdgcn_s_memrealtime())
-#define SI_TRACE_FLUSH                                                                            \
-  do {                                                                                            \
-    if (threadIdx.x == 0)                                                                         \
-      for (int si_s_ = 0; si_s_ < kTraceBlockMarks; ++si_s_)                                      \
-        g_si_trace[(size_t)blockIdx.x * kTraceSlots + si_s_] = si_tr_[si_s_];                     \
-    if ((threadIdx.x & 63) == 0)                                                                  \
-      for (int si_m_ = 0; si_m_ < kTraceWaveMarks; ++si_m_)                                       \
-        g_si_trace_wave[((size_t)blockIdx.x * 16 + (threadIdx.x >> 6)) * kTraceWaveMarks + si_m_] = \
-            si_trw_[si_m_];                                                                       \
+#define SI_TRACE_DECL                                                 \
+  __shared__ uint64_t si_tr_[kTraceBlockMarks + 16 * kTraceWaveMarks]; \
+  for (int si_i_ = threadIdx.x; si_i_ < kTraceBlockMarks + 16 * kTraceWaveMarks; si_i_ += blockDim.x) si_tr_[si_i_] = 0
+#define SI_TRACE_MARK(slot)                                               \
+  do {                                                                    \
+    if (threadIdx.x == 0) si_tr_[(slot)] = __builtin_amdgcn_s_memrealtime(); \
+  } while (0)
+#define SI_TRACE_WAVE(mark)                                                                                  \
+  do {                                                                                                       \
+    if ((threadIdx.x & 63) == 0)                                                                             \
+      si_tr_[kTraceBlockMarks + (threadIdx.x >> 6) * kTraceWaveMarks + (mark)] = __builtin_amdgcn_s_memrealtime(); \
+  } while (0)
+#define SI_TRACE_FLUSH                                                                                     \
+  do {                                                                                                     \
+    __syncthreads();                                                                                       \
+    if (threadIdx.x < kTraceBlockMarks)                                                                    \
+      g_si_trace[(size_t)blockIdx.x * kTraceSlots + threadIdx.x] = si_tr_[threadIdx.x];                    \
+    if (threadIdx.x < 16 * kTraceWaveMarks)                                                                \
+      g_si_trace_wave[(size_t)blockIdx.x * 16 * kTraceWaveMarks + threadIdx.x] =                           \
+          si_tr_[kTraceBlockMarks + threadIdx.x];                                                          \
   } while (0)
 #else
 #define SI_TRACE_DECL \

@@ -277,6 +277,28 @@ def test_batch_union(b):
         check_mlp(c, c.x, m_ref, y, cnt)
 
 
+@pytest.mark.parametrize("k,d,b", [(700, 8192, 5), (700, 8192, 8), (1500, 5120, 8), (1300, 4096, 7)])
+def test_batch_wide_rows(k, d, b):
+    """Batches of 5 to 8 tokens with the widest rows: the token block fills
+    most of the LDS and the per-token accumulators most of the registers."""
+    rng = np.random.default_rng(k * 13 + d + b)
+    c = Case(rand_bits(rng, (k, d), False), rand_bits(rng, (k, d), False), rand_bits(rng, (d, k), False),
+             rand_bits(rng, (b, d), False), max_batch=b)
+    for alpha in [1.0, math.inf]:
+        y, (mask, idx, n, cnt) = c.layer(to_dev(c.x), alpha, outputs=True)
+        torch.cuda.synchronize()
+        m_ref = check_predict(c, c.x, alpha)
+        assert np.array_equal(mask.cpu().numpy(), m_ref)
+        check_list(idx, n, m_ref)
+        check_mlp(c, c.x, m_ref, y, cnt)
+        # the list-driven and the mask-driven sparse MLP on the same rows
+        y1, c1 = c.layer.sparse_mlp(to_dev(c.x), mask, idx, n, counters=True)
+        y2, c2 = c.layer.sparse_mlp(to_dev(c.x), mask=mask, counters=True)
+        torch.cuda.synchronize()
+        check_mlp(c, c.x, m_ref, y1, c1)
+        check_mlp(c, c.x, m_ref, y2, c2)
+
+
 @pytest.mark.parametrize("k,d", [(1, 128), (63, 128), (65, 384), (129, 8192), (1000, 640), (1, 8192),
                                  (20000, 384), (65536, 128)])
 def test_sparse_mlp_edge_shapes(k, d):
@@ -329,13 +351,12 @@ def test_13b_layer():
 @pytest.mark.parametrize("k,d,b,one", [(11008, 4096, 1, 1), (13824, 5120, 1, 1), (1376, 512, 1, 1),
                                        (11008, 4096, 2, 1), (1, 128, 1, 1), (65536, 128, 1, 1),
                                        (11008, 4096, 3, 1), (11008, 4096, 8, 1), (13824, 5120, 8, 1),
-                                       (129, 8192, 4, 1), (129, 8192, 5, 0), (65537, 128, 1, 0),
-                                       (11008, 4096, 9, 0)])
+                                       (129, 8192, 4, 1), (129, 8192, 5, 1), (700, 8192, 8, 1),
+                                       (65537, 128, 1, 0), (11008, 4096, 9, 0)])
 def test_single_launch_path(k, d, b, one):
     """The shapes the parity tests use run the one-launch kernel (so its
     results are the ones checked); k above 65536 (256 rows per compute unit)
-    and batches of more than 4
-    tokens at d > 5120 take the two-launch path."""
+    takes the two-launch path, and batches above 8 are rejected."""
     assert si._lib.load().si_single_launch(k, d, b) == one
 
 
