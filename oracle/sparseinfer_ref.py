@@ -19,6 +19,9 @@ check by eye against the paper:
   declares row ``i`` sparse when ``alpha * N_pos < N_neg``.
 * Section IV-B 1): signs are packed 32 consecutive elements per 32-bit word,
   for the weights once at load time and for the input once per token.
+* Section III also names MLP blocks without step 2 (OPT, Falcon after
+  ReLUfication): ``relu_mlp`` is that non-gated form,
+  ``MLP(X) = ReLU(X W_fc1) W_down^T``, with the predictor on ``W_fc1``.
 * Section IV-B 3)/4): the sparse GEMVs skip predicted-sparse rows of
   ``W_gate``, ``W_up`` and ``W_down^T``; "actual sparsity" additionally skips
   rows whose gate output is exactly zero.  Skipping a row whose value is zero
@@ -55,6 +58,7 @@ __all__ = [
     "predict_rows",
     "active_rows",
     "sparse_mlp",
+    "relu_mlp",
     "dense_mlp",
     "gate_truly_positive",
     "prediction_quality",
@@ -213,6 +217,46 @@ def sparse_mlp(w_gate, w_up, w_down, x, mask):
         "n_gate": int(keep.size),
         "n_up": int((h1_kept > 0).any(axis=0).sum()),
         "n_down": int((h3_kept != 0).any(axis=0).sum()),
+    }
+
+
+def relu_mlp(w_fc1, w_down, x, mask):
+    """Non-gated ReLU MLP over the rows kept by ``mask``: the MLP block of
+    models without step 2 of Section III (no ``W_up``; e.g. OPT and Falcon
+    after ReLUfication), ``MLP(X) = ReLU(X W_fc1) W_down^T``.  The predictor
+    runs on the signs of ``W_fc1`` exactly as on ``W_gate`` (its ReLU output
+    is the one that is sparse), and rows whose ReLU output is zero skip
+    ``W_down^T`` (actual sparsity, Section IV-B).
+
+    ``w_fc1``: ``[k][d]`` fp16 bits; ``w_down``: ``[d][k]``; ``x``: ``[b][d]``.
+    Returns ``y`` (``[b][d]`` float64), ``g`` and ``h`` (``[b][k]``, 0 on
+    dropped rows), ``n_gate`` (rows whose ``W_fc1`` row is read), ``n_up``
+    (always 0: there is no ``W_up``) and ``n_down`` (rows with some
+    ``h != 0``).
+    """
+    w_fc1 = _as_u16(w_fc1)
+    w_down = _as_u16(w_down)
+    xs = np.atleast_2d(_as_u16(x))
+    k, d = w_fc1.shape
+    if w_down.shape != (d, k) or xs.shape[-1] != d:
+        raise ValueError("shape mismatch")
+    keep = active_rows(mask)
+    b = xs.shape[0]
+    X = fp16_to_f64(xs)                        # [b][d]
+    W1 = fp16_to_f64(w_fc1[keep])              # [n][d]
+    WdT = fp16_to_f64(w_down[:, keep]).T       # [n][d]: rows of W_down^T
+    g_kept = X @ W1.T
+    h_kept = np.maximum(g_kept, 0.0)           # sigma = ReLU
+    y = h_kept @ WdT
+    g = np.zeros((b, k)); h = np.zeros((b, k))
+    g[:, keep] = g_kept; h[:, keep] = h_kept
+    return {
+        "y": y,
+        "g": g,
+        "h": h,
+        "n_gate": int(keep.size),
+        "n_up": 0,
+        "n_down": int((h_kept != 0).any(axis=0).sum()),
     }
 
 

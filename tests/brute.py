@@ -80,6 +80,24 @@ def mlp(w_gate, w_up, w_down, x, mask):
     return ys, gs, hs
 
 
+def relu_mlp(w_fc1, w_down, x, mask):
+    """Exact non-gated ReLU MLP over the kept rows (``w_down`` is
+    ``[d][k]``).  Returns ``(y[b][d], h[b][k])`` as Fractions."""
+    k, d = len(w_fc1), len(w_fc1[0])
+    ys, hs = [], []
+    for xt in x:
+        X = [Fraction(f16(v)) for v in xt]
+        h_t = [Fraction(0)] * k
+        for i in range(k):
+            if mask[i]:
+                g = sum((Fraction(f16(w_fc1[i][j])) * X[j] for j in range(d)), Fraction(0))
+                h_t[i] = max(g, Fraction(0))
+        ys.append([sum((h_t[i] * Fraction(f16(w_down[c][i])) for i in range(k)), Fraction(0))
+                   for c in range(d)])
+        hs.append(h_t)
+    return ys, hs
+
+
 def gate_positive(w_gate, x):
     """Exact ``X . W_gate,i > 0`` for every token and row."""
     out = []

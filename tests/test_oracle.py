@@ -387,3 +387,85 @@ def test_exactly_zero_gate_is_not_counted_as_up_work():
     # row 1: h1 = 1 but u = 0 -> h3 = 0 -> W_down^T row skipped
     assert (out["n_gate"], out["n_up"], out["n_down"]) == (3, 1, 0)
     assert np.all(out["y"] == 0)
+
+
+# ---------------------------------------------------------------------------
+# The non-gated ReLU MLP (Section III: blocks without step 2)
+# ---------------------------------------------------------------------------
+
+def test_relu_mlp_golden_example():
+    lines = list(_golden_lines("relu_mlp_worked_example.txt"))
+    def mat(tokens):
+        return [list(map(float, part.split())) for part in " ".join(tokens).split("|")]
+    rec = {l[0]: l[1:] for l in lines if l[0] != "case"}
+    x = _bits(map(float, rec["x"]))[None, :]
+    w1 = np.stack([_bits(r) for r in mat(rec["fc1"])])
+    wd = np.stack([_bits(r) for r in mat(rec["down"])])
+    h_all = list(map(float, rec["h"]))
+    for l in lines:
+        if l[0] != "case":
+            continue
+        arrow = l.index("->")
+        mask = np.array(list(map(int, l[1:arrow])), dtype=np.uint8)
+        y0, y1, ng, nd = map(float, l[arrow + 1:])
+        out = oracle.relu_mlp(w1, wd, x, mask)
+        assert out["y"][0].tolist() == [y0, y1]
+        assert (out["n_gate"], out["n_up"], out["n_down"]) == (ng, 0, nd)
+        assert out["h"][0].tolist() == [h if m else 0.0 for h, m in zip(h_all, mask)]
+
+
+@pytest.mark.parametrize("k,d,b", [(5, 3, 1), (17, 8, 2), (33, 16, 1), (24, 40, 3)])
+def test_relu_mlp_matches_exact_rationals(k, d, b):
+    rng = np.random.default_rng(k * 100 + d + 7)
+    w1 = _random_bits(rng, (k, d), special=False)
+    wd = _random_bits(rng, (d, k), special=False)
+    x = _random_bits(rng, (b, d), special=False)
+    for mask in [np.ones(k, np.uint8), np.zeros(k, np.uint8), (rng.random(k) < 0.4).astype(np.uint8)]:
+        out = oracle.relu_mlp(w1, wd, x, mask)
+        y, h = brute.relu_mlp(w1.tolist(), wd.tolist(), x.tolist(), mask.tolist())
+        for t in range(b):
+            scale = max(1e-300, max(abs(float(v)) for v in y[t]))
+            for c in range(d):
+                assert abs(out["y"][t, c] - float(y[t][c])) <= 1e-12 * scale
+            for i in range(k):
+                assert abs(out["h"][t, i] - float(h[t][i])) <= 1e-12 * max(1.0, abs(float(h[t][i])))
+        assert out["n_gate"] == int(mask.sum())
+        assert out["n_down"] == sum(1 for i in range(k) if mask[i] and any(h[t][i] != 0 for t in range(b)))
+
+
+def test_relu_mlp_is_the_gated_mlp_with_unit_up():
+    """With x_0 = 1 in every token and every W_up row the unit vector e_0,
+    u = 1 exactly, so the gated MLP of Eq. (1) reduces to the non-gated one
+    (h3 = ReLU(g) * 1)."""
+    rng = np.random.default_rng(11)
+    k, d, b = 40, 24, 3
+    w1 = _random_bits(rng, (k, d), special=False)
+    wd = _random_bits(rng, (d, k), special=False)
+    x = _random_bits(rng, (b, d), special=False)
+    x[:, 0] = brute.fp16_bits(1.0)
+    wu = np.zeros((k, d), dtype=np.uint16)
+    wu[:, 0] = brute.fp16_bits(1.0)
+    for mask in [np.ones(k, np.uint8), (rng.random(k) < 0.5).astype(np.uint8)]:
+        gated = oracle.sparse_mlp(w1, wu, wd, x, mask)
+        plain = oracle.relu_mlp(w1, wd, x, mask)
+        assert np.array_equal(gated["u"][:, mask.astype(bool)], np.ones((b, int(mask.sum()))))
+        assert np.array_equal(gated["y"], plain["y"])
+        assert np.array_equal(gated["h3"], plain["h"])
+        assert gated["n_down"] == plain["n_down"]
+
+
+def test_relu_mlp_superset_of_positive_rows_equals_dense():
+    """Dropping only rows whose ReLU output is zero for every token leaves y
+    unchanged (the exact truth decides which rows those are)."""
+    rng = np.random.default_rng(12)
+    k, d, b = 64, 32, 2
+    w1 = _random_bits(rng, (k, d), special=False)
+    wd = _random_bits(rng, (d, k), special=False)
+    x = _random_bits(rng, (b, d), special=False)
+    pos = oracle.gate_truly_positive(w1, x).any(axis=0)
+    dense = oracle.relu_mlp(w1, wd, x, np.ones(k, np.uint8))
+    extra = (rng.random(k) < 0.3)
+    part = oracle.relu_mlp(w1, wd, x, (pos | extra).astype(np.uint8))
+    assert np.allclose(part["y"], dense["y"], rtol=1e-12, atol=0)
+    none = oracle.relu_mlp(w1, wd, x, np.zeros(k, np.uint8))
+    assert np.all(none["y"] == 0)
