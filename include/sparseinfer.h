@@ -156,12 +156,12 @@ si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint
                         void* stream);
 
 /*
- * 1 if si_predict, si_sparse_mlp and si_predict_sparse_mlp run as a single
- * kernel launch for these shapes on the current device: at most 256 rows of
- * W_gate per compute unit (k <= 65536 on a 256-CU MI355X), b <= 8 (b <= 4
- * when d > 5120), and one 1024-thread block with 96-160 KB of LDS resident
- * on every compute unit; 0 if they take the multi-launch path (same results)
- * or the shapes are invalid.  Host-only query.
+ * 1 if si_predict, si_sparse_mlp and si_predict_sparse_mlp (and their
+ * non-gated forms) run as a single kernel launch for these shapes on the
+ * current device: at most 256 rows of W_gate per compute unit (k <= 65536 on
+ * a 256-CU MI355X) and one block with 96-160 KB of LDS resident on every
+ * compute unit; 0 if they take the multi-launch path (same results) or the
+ * shapes are invalid.  Host-only query.
  */
 int si_single_launch(int k, int d, int b);
 
@@ -175,6 +175,31 @@ si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, c
                                 float alpha, uint8_t* mask, int32_t* active_idx, int32_t* n_active,
                                 float* y, void* workspace, size_t workspace_bytes, uint32_t flags,
                                 int32_t* counters, void* stream);
+
+/*
+ * Non-gated ReLU MLP: the MLP block of models without step 2 of Section III
+ * (no W_up; e.g. OPT and Falcon after ReLUfication):
+ *   MLP(X) = ReLU(X W_fc1) W_down^T.
+ * For every kept row i and token t: g = W_fc1,i . x_t ; h = max(g, 0) ;
+ * y_t += h * W_down^T[i, :] (row read only when some token has h != 0).
+ * Arguments, outputs, flags and errors as si_sparse_mlp, with w_fc1 [k][d]
+ * fp16 in place of w_gate and no w_up; counters[1] (n_up) is always 0.
+ * The predictor runs on the signs of W_fc1 (si_pack_signs(w_fc1)).
+ */
+si_status si_sparse_relu_mlp(const uint16_t* w_fc1, const uint16_t* w_down_t, int k, int d, const uint16_t* x,
+                             int b, const uint8_t* mask, const int32_t* active_idx, const int32_t* n_active,
+                             float* y, void* workspace, size_t workspace_bytes, uint32_t flags, int32_t* counters,
+                             void* stream);
+
+/*
+ * The whole per-token path of the non-gated ReLU MLP: si_predict on the
+ * signs of W_fc1 followed by si_sparse_relu_mlp, with the arguments and
+ * outputs of si_predict_sparse_mlp (no w_up).
+ */
+si_status si_predict_sparse_relu_mlp(const uint32_t* signs, const uint16_t* w_fc1, const uint16_t* w_down_t, int k,
+                                     int d, const uint16_t* x, int b, float alpha, uint8_t* mask,
+                                     int32_t* active_idx, int32_t* n_active, float* y, void* workspace,
+                                     size_t workspace_bytes, uint32_t flags, int32_t* counters, void* stream);
 
 #ifdef __cplusplus
 }

@@ -125,24 +125,31 @@ def predict(signs: torch.Tensor, x: torch.Tensor, alpha: float, k: int, workspac
 def sparse_mlp(w_gate, w_up, w_down_t, x, workspace, mask=None, active_idx=None, n_active=None,
                flags: int = 0, counters: bool = False):
     """Eq. (1) over the kept rows; returns ``y [b][d]`` float32 (and the
-    ``[3]`` work counters when ``counters``)."""
+    ``[3]`` work counters when ``counters``).  ``w_up=None`` runs the
+    non-gated ReLU MLP ``ReLU(x W_fc1) W_down^T`` with ``w_gate`` as
+    ``W_fc1`` (``si_sparse_relu_mlp``)."""
     for t, nm in ((w_gate, "w_gate"), (w_up, "w_up"), (w_down_t, "w_down_t")):
-        _dev(t, nm, _F16, 2)
+        if t is not None or nm != "w_up":
+            _dev(t, nm, _F16, 2)
     k, d = w_gate.shape
     x = _x2(x, d)
     b = x.shape[0]
     y = torch.empty(b, d, dtype=torch.float32, device=x.device)
     cnt = torch.zeros(3, dtype=torch.int32, device=x.device) if counters else None
-    _lib.call("si_sparse_mlp", _vp(w_gate), _vp(w_up), _vp(w_down_t), k, d, _vp(x), b, _vp(mask),
-              _vp(active_idx), _vp(n_active), _vp(y), _vp(workspace), workspace.numel(), flags, _vp(cnt),
-              _stream())
+    tail = (k, d, _vp(x), b, _vp(mask), _vp(active_idx), _vp(n_active), _vp(y), _vp(workspace),
+            workspace.numel(), flags, _vp(cnt), _stream())
+    if w_up is None:
+        _lib.call("si_sparse_relu_mlp", _vp(w_gate), _vp(w_down_t), *tail)
+    else:
+        _lib.call("si_sparse_mlp", _vp(w_gate), _vp(w_up), _vp(w_down_t), *tail)
     return (y, cnt) if counters else y
 
 
 def predict_sparse_mlp(signs, w_gate, w_up, w_down_t, x, alpha, workspace, flags: int = 0,
                        outputs: bool = False, y: torch.Tensor = None):
     """The whole per-token path.  Returns ``y`` (written into ``y`` when
-    given); with ``outputs`` also ``(mask, active_idx, n_active, counters)``."""
+    given); with ``outputs`` also ``(mask, active_idx, n_active, counters)``.
+    ``w_up=None``: the non-gated ReLU MLP (``si_predict_sparse_relu_mlp``)."""
     k, d = w_gate.shape
     x = _x2(x, d)
     b = x.shape[0]
@@ -159,15 +166,20 @@ def predict_sparse_mlp(signs, w_gate, w_up, w_down_t, x, alpha, workspace, flags
         cnt = torch.zeros(3, dtype=torch.int32, device=x.device)
     else:
         mask = idx = n = cnt = None
-    _lib.call("si_predict_sparse_mlp", _vp(signs), _vp(w_gate), _vp(w_up), _vp(w_down_t), k, d, _vp(x), b,
-              float(alpha), _vp(mask), _vp(idx), _vp(n), _vp(y), _vp(workspace), workspace.numel(), flags,
-              _vp(cnt), _stream())
+    tail = (k, d, _vp(x), b, float(alpha), _vp(mask), _vp(idx), _vp(n), _vp(y), _vp(workspace),
+            workspace.numel(), flags, _vp(cnt), _stream())
+    if w_up is None:  # the non-gated ReLU MLP, w_gate as W_fc1
+        _lib.call("si_predict_sparse_relu_mlp", _vp(signs), _vp(w_gate), _vp(w_down_t), *tail)
+    else:
+        _lib.call("si_predict_sparse_mlp", _vp(signs), _vp(w_gate), _vp(w_up), _vp(w_down_t), *tail)
     return (y, (mask, idx, n, cnt)) if outputs else y
 
 
 class MLPLayer:
     """One layer's device-resident state: weights, packed signs and
-    ``W_down^T`` (both made once at load), plus a workspace."""
+    ``W_down^T`` (both made once at load), plus a workspace.  With
+    ``w_up=None`` the layer is a non-gated ReLU MLP and ``w_gate`` is its
+    ``W_fc1``."""
 
     def __init__(self, w_gate: torch.Tensor, w_up: torch.Tensor, w_down: torch.Tensor, max_batch: int = 1,
                  keep_w_down: bool = False):

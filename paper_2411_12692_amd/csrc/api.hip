@@ -164,12 +164,16 @@ si_status si_predict(const uint32_t* signs, int k, int d, const uint16_t* x, int
                     "predict launch");
 }
 
-si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint16_t* w_down_t, int k, int d,
-                        const uint16_t* x, int b, const uint8_t* mask, const int32_t* active_idx,
-                        const int32_t* n_active, float* y, void* workspace, size_t workspace_bytes,
-                        uint32_t flags, int32_t* counters, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// si_sparse_mlp and si_sparse_relu_mlp (w_up == nullptr: no W_up).
+si_status sparse_mlp_impl(const uint16_t* w_gate, const uint16_t* w_up, const uint16_t* w_down_t, int k, int d,
+                          const uint16_t* x, int b, const uint8_t* mask, const int32_t* active_idx,
+                          const int32_t* n_active, float* y, void* workspace, size_t workspace_bytes,
+                          uint32_t flags, int32_t* counters, void* stream) {
   REQUIRE_PTR(w_gate);
-  REQUIRE_PTR(w_up);
   REQUIRE_PTR(w_down_t);
   REQUIRE_PTR(x);
   REQUIRE_PTR(y);
@@ -226,13 +230,13 @@ si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint
                     "sparse_mlp launch");
 }
 
-si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, const uint16_t* w_up,
-                                const uint16_t* w_down_t, int k, int d, const uint16_t* x, int b, float alpha,
-                                uint8_t* mask, int32_t* active_idx, int32_t* n_active, float* y, void* workspace,
-                                size_t workspace_bytes, uint32_t flags, int32_t* counters, void* stream) {
+// si_predict_sparse_mlp and si_predict_sparse_relu_mlp (w_up == nullptr).
+si_status predict_sparse_mlp_impl(const uint32_t* signs, const uint16_t* w_gate, const uint16_t* w_up,
+                                  const uint16_t* w_down_t, int k, int d, const uint16_t* x, int b, float alpha,
+                                  uint8_t* mask, int32_t* active_idx, int32_t* n_active, float* y, void* workspace,
+                                  size_t workspace_bytes, uint32_t flags, int32_t* counters, void* stream) {
   REQUIRE_PTR(signs);
   REQUIRE_PTR(w_gate);
-  REQUIRE_PTR(w_up);
   REQUIRE_PTR(w_down_t);
   REQUIRE_PTR(x);
   REQUIRE_PTR(y);
@@ -286,6 +290,44 @@ si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, c
   return hip_status(si::launch_down(w_down_t, k, d, b, active_idx, n_active, y, workspace, si::row_groups(k), flags,
                                     counters, st),
                     "down-projection launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint16_t* w_down_t, int k, int d,
+                        const uint16_t* x, int b, const uint8_t* mask, const int32_t* active_idx,
+                        const int32_t* n_active, float* y, void* workspace, size_t workspace_bytes,
+                        uint32_t flags, int32_t* counters, void* stream) {
+  REQUIRE_PTR(w_up);
+  return sparse_mlp_impl(w_gate, w_up, w_down_t, k, d, x, b, mask, active_idx, n_active, y, workspace,
+                         workspace_bytes, flags, counters, stream);
+}
+
+si_status si_sparse_relu_mlp(const uint16_t* w_fc1, const uint16_t* w_down_t, int k, int d, const uint16_t* x,
+                             int b, const uint8_t* mask, const int32_t* active_idx, const int32_t* n_active,
+                             float* y, void* workspace, size_t workspace_bytes, uint32_t flags, int32_t* counters,
+                             void* stream) {
+  return sparse_mlp_impl(w_fc1, nullptr, w_down_t, k, d, x, b, mask, active_idx, n_active, y, workspace,
+                         workspace_bytes, flags, counters, stream);
+}
+
+si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, const uint16_t* w_up,
+                                const uint16_t* w_down_t, int k, int d, const uint16_t* x, int b, float alpha,
+                                uint8_t* mask, int32_t* active_idx, int32_t* n_active, float* y, void* workspace,
+                                size_t workspace_bytes, uint32_t flags, int32_t* counters, void* stream) {
+  REQUIRE_PTR(w_up);
+  return predict_sparse_mlp_impl(signs, w_gate, w_up, w_down_t, k, d, x, b, alpha, mask, active_idx, n_active, y,
+                                 workspace, workspace_bytes, flags, counters, stream);
+}
+
+si_status si_predict_sparse_relu_mlp(const uint32_t* signs, const uint16_t* w_fc1, const uint16_t* w_down_t, int k,
+                                     int d, const uint16_t* x, int b, float alpha, uint8_t* mask,
+                                     int32_t* active_idx, int32_t* n_active, float* y, void* workspace,
+                                     size_t workspace_bytes, uint32_t flags, int32_t* counters, void* stream) {
+  return predict_sparse_mlp_impl(signs, w_fc1, nullptr, w_down_t, k, d, x, b, alpha, mask, active_idx, n_active,
+                                 y, workspace, workspace_bytes, flags, counters, stream);
 }
 
 }  // extern "C"

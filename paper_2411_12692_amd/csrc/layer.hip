@@ -53,7 +53,7 @@ constexpr int kMaxSlice = 256;             // gate/up positions of one block (at
 
 struct LayerArgs {
   const u32x4* wg;
-  const u32x4* wu;
+  const u32x4* wu;  // nullptr: the non-gated ReLU MLP (h3 = ReLU(g))
   const u32x4* wdt;
   const uint16_t* x;
   const int32_t* idx_in;  // the caller's ascending kept rows
@@ -111,6 +111,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
   const int T = a.tiles;
   const bool no_as = (a.flags & kNoAS) != 0;
   const bool spec_ok = (a.flags & kNoSpec) == 0;
+  const bool gated = a.wu != nullptr;  // else the non-gated ReLU MLP (no W_up)
 
   SI_TRACE_DECL;
   SI_TRACE_MARK(0);
@@ -223,7 +224,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
     // the row's requests and their use sit in one branch, so that no request
     // is left outstanding across rounds (the compiler then issues them back
     // to back instead of waiting before each)
-    if (e != kBadRow && (imat == 0 || (spec_ok && (e >> 31)))) {
+    if (e != kBadRow && (imat == 0 || (gated && spec_ok && (e >> 31)))) {
       u32x4 v[NU];
       load_row<NU>((imat ? a.wu : a.wg) + (size_t)(e & 0x7fffffffu) * U, U, lane, v);
       SI_TRACE_WAVE(0);
@@ -250,8 +251,8 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
           L.h1[lane][t] = h;
           any |= h > 0.f;
         }
-        any = any && ok;
-        spec = ok && spec_ok && (srow[lane] >> 31);
+        any = any && ok && gated;  // W_up rows exist only in the gated MLP
+        spec = ok && gated && spec_ok && (srow[lane] >> 31);
         L.need[lane] = (any && !spec) ? 1u : 0u;
       }
       const uint64_t late = __ballot(lane < mr && any && !spec);
@@ -278,7 +279,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
     for (int i = tid; i < mr * b; i += kLThreads) {
       const int r = i / b, t = i - r * b;
       const bool spec = srow[r] != kBadRow && spec_ok && (srow[r] >> 31);
-      const float h = (L.need[r] || spec) ? L.h1[r][t] * L.dots[r][1][t] : 0.f;
+      const float h = !gated ? L.h1[r][t] : (L.need[r] || spec) ? L.h1[r][t] * L.dots[r][1][t] : 0.f;
       st_agent64(&a.h3e[(size_t)(r0 + r) * b + t], tagged(tag, __float_as_uint(h)));
     }
   }

@@ -81,7 +81,7 @@ static_assert(kODN * kMaxB <= kWave, "a wave polls the h3 words of its pieces, o
 struct OwnedArgs {
   const u32x4* signs;
   const u32x4* wg;
-  const u32x4* wu;
+  const u32x4* wu;         // nullptr: the non-gated ReLU MLP (h3 = ReLU(g))
   const u32x4* wdt;
   const uint16_t* x;
   const uint8_t* mask_in;  // mask mode (else predict mode)
@@ -238,6 +238,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   const bool predict = a.mask_in == nullptr;
   const bool no_as = (a.flags & kNoAS) != 0;
   const bool spec_ok = (a.flags & kNoSpec) == 0;
+  const bool gated = a.wu != nullptr;  // else the non-gated ReLU MLP (no W_up)
   const bool owns_tile = a.mlp && blk < T;
 
   SI_TRACE_DECL;
@@ -461,7 +462,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       float g[BM], u[BM];
       bool up;
       // a row's requests and their use sit in one branch (row-uniform)
-      if ((spec_ok && (e >> 31)) || no_as) {
+      if (gated && ((spec_ok && (e >> 31)) || no_as)) {
         u32x4 vg[NU], vu[NU];
         load_row<NU>(a.wg + (size_t)row * U, U, lane, vg);
         load_row<NU>(a.wu + (size_t)row * U, U, lane, vu);
@@ -475,14 +476,14 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         bool any = false;
 #pragma unroll
         for (int t = 0; t < BM; ++t) any |= g[t] > 0.f;
-        up = any;
-        if (any) {
+        up = gated && any;
+        if (up) {
           u32x4 vu[NU];
           load_row<NU>(a.wu + (size_t)row * U, U, lane, vu);
           row_dots<BM, NU>(vu, L.xs, U, lane, u);
-        } else {
+        } else {  // h3 = ReLU(g) * 1 without W_up
 #pragma unroll
-          for (int t = 0; t < BM; ++t) u[t] = 0.f;
+          for (int t = 0; t < BM; ++t) u[t] = gated ? 0.f : 1.f;
         }
       }
       n_up += up ? 1 : 0;

@@ -177,7 +177,9 @@ __device__ inline void row_dot(const u32x4* __restrict__ row, const u32x4* xs, i
 // Gate/up of one kept row (Eq. (1) steps 1-3 with actual sparsity): returns
 // through h[] the B values h3 = ReLU(W_gate,row . x) * (W_up,row . x); the
 // W_up row is read only if some token has a positive gate value (or always
-// with no_as).  Stores h3 per row, the up-read flag, and counts the work.
+// with no_as).  Without W_up (wu == nullptr: the non-gated ReLU MLP of
+// blocks without step 2) h3 = ReLU(W_gate,row . x).  Stores h3 per row, the
+// up-read flag, and counts the work.
 template <int B>
 __device__ inline void gate_up_row(const u32x4* __restrict__ wg, const u32x4* __restrict__ wu, int row, int U,
                                    const u32x4* xs, int lane, bool no_as, float* __restrict__ h3row,
@@ -193,12 +195,16 @@ __device__ inline void gate_up_row(const u32x4* __restrict__ wg, const u32x4* __
   float h[B];
 #pragma unroll
   for (int t = 0; t < B; ++t) h[t] = 0.f;
-  const bool up = any || no_as;
+  const bool gated = wu != nullptr;
+  const bool up = gated && (any || no_as);
   if (up) {
     float u[B];
     row_dot<B>(wu + (size_t)row * U, xs, U, lane, u);
 #pragma unroll
     for (int t = 0; t < B; ++t) h[t] = g[t] * u[t];
+  } else if (!gated) {
+#pragma unroll
+    for (int t = 0; t < B; ++t) h[t] = g[t];
   }
   bool nz = false;
 #pragma unroll
