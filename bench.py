@@ -4,6 +4,8 @@ One step = one pass of the whole per-token path over one layer: x-sign
 packing, sign-bit prediction (Eq. (2)), compaction, sparse gate/up with
 actual sparsity and sparse down-projection, for the 7B-shaped layer
 (d = 4096, k = 11008) with planted sparsity s = 0.9, alpha = 1.0, batch 1.
+``--mlp relu`` times the non-gated ReLU MLP (no W_up) of an OPT-6.7B-shaped
+layer (d = 4096, k = 16384) instead, same sparsity and alpha.
 Steps cycle through a pool of independently seeded layers whose weights
 (>= 4.4 GB) exceed the 256 MB Infinity Cache, so every step reads its bytes
 from HBM.  The timed loop is replayed from a HIP graph (the per-call host
@@ -31,6 +33,9 @@ if ROOT not in sys.path:
 METRIC = "µs per MLP layer (predict+sparse GEMV) at 7B shape, s=0.9; effective HBM GB/s"
 D, K, S = 4096, 11008, 0.9
 HBM_PEAK_GBS = 8000.0
+# the non-gated workload (--mlp relu): OPT-6.7B's MLP shape
+RELU_METRIC = "µs per non-gated ReLU MLP layer (predict+sparse GEMV) at OPT-6.7B shape, s=0.9; effective HBM GB/s"
+RELU_D, RELU_K = 4096, 16384
 
 
 def algorithmic_bytes(k, d, b, n_gate, n_up, n_down):
@@ -39,6 +44,7 @@ def algorithmic_bytes(k, d, b, n_gate, n_up, n_down):
 
 
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_7b_s0.9_counters.txt")
+RELU_COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_opt6.7b_relu_s0.9_counters.txt")
 KERNEL_SOURCES = ("paper_2411_12692_amd/csrc/owned.hip", "paper_2411_12692_amd/csrc/layer_common.h",
                   "paper_2411_12692_amd/csrc/si_device.h")
 
@@ -53,11 +59,11 @@ def kernel_sources_sha256():
     return h.hexdigest()
 
 
-def measured_traffic():
+def measured_traffic(counters_file=COUNTERS_FILE):
     """HBM bytes per k_owned launch from the committed FETCH_SIZE/WRITE_SIZE
     summary, or None when that summary was taken on other kernel sources."""
     try:
-        with open(COUNTERS_FILE) as f:
+        with open(counters_file) as f:
             fields = dict(line.split(":", 1) for line in f if ":" in line and not line.startswith((" ", "#", "|")))
     except OSError:
         return None
@@ -77,6 +83,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=256)
     ap.add_argument("--layers", type=int, default=16, help="size of the rotating layer pool")
     ap.add_argument("--alpha", type=float, default=1.0)
+    ap.add_argument("--mlp", choices=("gated", "relu"), default="gated",
+                    help="gated: the 7B-shaped gated MLP (default); relu: the non-gated ReLU MLP of an "
+                         "OPT-6.7B-shaped layer")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--launches", type=int, default=256, help="individually timed launches for the roofline")
@@ -103,10 +112,11 @@ def profile_pass(layers, xs, ys, alpha, calls):
     print(f"# profile pass: {calls} layer calls, 4 copies of {src.numel() * 2} bytes", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(layers_host, alpha, budget_s):
+def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D):
     """Time the CPU oracle (test infrastructure, never tuned) on a bounded
     sample of the same workload: predict + masked MLP on the first layers of
-    the pool, repeated until the budget is spent, with one BLAS thread."""
+    the pool, repeated until the budget is spent, with one BLAS thread
+    (``wu is None``: the non-gated MLP)."""
     import numpy as np
     from threadpoolctl import threadpool_limits
 
@@ -118,10 +128,13 @@ def cpu_baseline(layers_host, alpha, budget_s):
             for wg, wu, wd, x, packed in layers_host:
                 t0 = time.perf_counter()
                 mask, _, _ = oracle.predict_rows(packed, x, alpha)
-                out = oracle.sparse_mlp(wg, wu, wd, x, mask)
+                if wu is None:
+                    out = oracle.relu_mlp(wg, wd, x, mask)
+                else:
+                    out = oracle.sparse_mlp(wg, wu, wd, x, mask)
                 total_s += time.perf_counter() - t0
                 calls += 1
-                total_bytes += algorithmic_bytes(K, D, x.shape[0], out["n_gate"], out["n_up"], out["n_down"])
+                total_bytes += algorithmic_bytes(k, d, x.shape[0], out["n_gate"], out["n_up"], out["n_down"])
                 if total_s >= budget_s:
                     break
     return {
@@ -131,7 +144,8 @@ def cpu_baseline(layers_host, alpha, budget_s):
         "cores": 1,
         "kind": "oracle",
         "sample": f"{calls} layer calls over the first {len(layers_host)} layers of the pool "
-                  f"(predict_rows + sparse_mlp, numpy float64, 1 thread, {total_s:.1f} s)",
+                  f"(predict_rows + {'relu_mlp' if layers_host[0][1] is None else 'sparse_mlp'}, "
+                  f"numpy float64, 1 thread, {total_s:.1f} s)",
         "cpu": platform.processor() or platform.machine(),
     }
 
@@ -158,16 +172,20 @@ def main():
     torch.cuda.set_device(dev)
     si._lib.load()  # fails loudly if the library is not built
 
+    relu = args.mlp == "relu"
+    D_, K_ = (RELU_D, RELU_K) if relu else (D, K)
     L = args.layers
     layers, xs, host = [], [], []
     for l in range(L):
-        pl = synth.planted_layer(D, K, S, config=2, layer=l, device=dev)
-        layers.append(si.MLPLayer(pl.w_gate, pl.w_up, pl.w_down))
+        # the non-gated layer takes the planted W_gate as its W_fc1
+        pl = synth.planted_layer(D_, K_, S, config=7 if relu else 2, layer=l, device=dev)
+        layers.append(si.MLPLayer(pl.w_gate, None if relu else pl.w_up, pl.w_down))
         xs.append(pl.x)
         if not args.no_cpu_baseline and l < 2:
             def u16(t):
                 return t.cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
-            wg, wu, wd, xh = u16(pl.w_gate), u16(pl.w_up), u16(pl.w_down), u16(pl.x)
+            wg, wd, xh = u16(pl.w_gate), u16(pl.w_down), u16(pl.x)
+            wu = None if relu else u16(pl.w_up)
             import oracle
             host.append((wg, wu, wd, xh, oracle.pack_signs(wg)))
         del pl
@@ -175,7 +193,7 @@ def main():
     print(f"# pool of {L} layers ready", file=sys.stderr, flush=True)
 
     # per-layer work counters (deterministic per layer) -> algorithmic bytes
-    ys = [torch.empty(1, D, dtype=torch.float32, device=dev) for _ in range(L)]
+    ys = [torch.empty(1, D_, dtype=torch.float32, device=dev) for _ in range(L)]
     counts = []
     for l in range(L):
         _, (_, _, _, c) = layers[l](xs[l], args.alpha, outputs=True, y=ys[l])
@@ -185,7 +203,7 @@ def main():
     if args.profile_pass:
         profile_pass(layers, xs, ys, args.alpha, max(args.launches, L))
         return
-    bytes_per_layer = [algorithmic_bytes(K, D, 1, *c) for c in counts]
+    bytes_per_layer = [algorithmic_bytes(K_, D_, 1, *c) for c in counts]
     mean_bytes = sum(bytes_per_layer) / L
 
     # graph of one pass over the pool, replayed
@@ -240,7 +258,7 @@ def main():
     isolated_us = sum(a.elapsed_time(b) * 1e3 for a, b in evs) / M
 
     result = {
-        "metric": METRIC,
+        "metric": RELU_METRIC if relu else METRIC,
         "value": round(mean_bytes / us_per_layer / 1e3, 2),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -255,9 +273,11 @@ def main():
         "accumulate": "f32",
         "data": "synthetic",
         "config": {
-            "workload": f"7B-shaped ReLU gated MLP layer d={D} k={K}, planted sparsity s={S}, alpha={args.alpha}, "
-                        f"batch 1, rotating pool of {L} layers, HIP-graph replay",
-            "d": D, "k": K, "batch": 1, "alpha": args.alpha, "layers_in_pool": L,
+            "workload": (f"OPT-6.7B-shaped non-gated ReLU MLP layer (no W_up) d={D_} k={K_}" if relu else
+                         f"7B-shaped ReLU gated MLP layer d={D_} k={K_}") +
+                        f", planted sparsity s={S}, alpha={args.alpha}, batch 1, rotating pool of {L} layers, "
+                        f"HIP-graph replay",
+            "d": D_, "k": K_, "batch": 1, "alpha": args.alpha, "layers_in_pool": L,
             "kept_rows": [c[0] for c in counts[:4]],
             "bytes_per_layer": int(mean_bytes),
         },
@@ -268,13 +288,13 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(),
+            "traffic": measured_traffic(RELU_COUNTERS_FILE if relu else COUNTERS_FILE),
             "launch_us": round(us_per_layer, 3),
             "isolated_launch_us": round(isolated_us, 3),
         },
     }
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(host, args.alpha, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(host, args.alpha, args.cpu_seconds, K_, D_)
     print(json.dumps(result), flush=True)
 
 
