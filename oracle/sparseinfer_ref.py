@@ -59,6 +59,8 @@ __all__ = [
     "active_rows",
     "sparse_mlp",
     "relu_mlp",
+    "rmsnorm_fp16",
+    "mlp_block",
     "dense_mlp",
     "gate_truly_positive",
     "prediction_quality",
@@ -258,6 +260,40 @@ def relu_mlp(w_fc1, w_down, x, mask):
         "n_up": 0,
         "n_down": int((h_kept != 0).any(axis=0).sum()),
     }
+
+
+def rmsnorm_fp16(h, w_norm, eps: float) -> np.ndarray:
+    """The input of the MLP in a decoder layer: ``x = RMSNorm(h) * w_norm``,
+    ``x_j = h_j / sqrt(mean_j(h_j^2) + eps) * w_j`` per token, computed in
+    float64 and rounded to fp16 (round to nearest even), returned as fp16
+    bits ``[b][d]``.  ``h`` (the residual stream) and ``w_norm`` are float32
+    values.  This is the neighbour of the path that produces ``X``; the
+    paper packs the signs of ``X`` during decode (Section IV-B 1), so a
+    kernel that forms ``X`` can form its sign words too."""
+    H = np.atleast_2d(np.asarray(h, dtype=np.float32)).astype(np.float64)
+    Wn = np.asarray(w_norm, dtype=np.float32).astype(np.float64)
+    if H.shape[-1] != Wn.shape[0]:
+        raise ValueError("shape mismatch")
+    ms = np.mean(H * H, axis=1, keepdims=True)
+    X = H / np.sqrt(ms + float(np.float32(eps))) * Wn[None, :]
+    return X.astype(np.float16).view(np.uint16)
+
+
+def mlp_block(h, w_norm, eps: float, packed_w, w_gate, w_up, w_down, alpha: float):
+    """The MLP half of a decoder layer around the path: ``x = RMSNorm(h) *
+    w_norm`` (fp16), the prediction on ``x``, the MLP over the kept rows
+    (gated, or non-gated when ``w_up`` is None), and the residual:
+    ``y = h + MLP(x)``.  Returns a dict with ``x`` (fp16 bits), ``mask``,
+    ``y`` (float64) and the MLP's outputs."""
+    x = rmsnorm_fp16(h, w_norm, eps)
+    mask, act, counts = predict_rows(packed_w, x, alpha)
+    out = relu_mlp(w_gate, w_down, x, mask) if w_up is None else sparse_mlp(w_gate, w_up, w_down, x, mask)
+    out = dict(out)
+    out["mlp_y"] = out["y"]
+    out["y"] = np.atleast_2d(np.asarray(h, dtype=np.float32)).astype(np.float64) + out["mlp_y"]
+    out["x"] = x
+    out["mask"] = mask
+    return out
 
 
 def dense_mlp(w_gate, w_up, w_down, x):

@@ -469,3 +469,64 @@ def test_relu_mlp_superset_of_positive_rows_equals_dense():
     assert np.allclose(part["y"], dense["y"], rtol=1e-12, atol=0)
     none = oracle.relu_mlp(w1, wd, x, np.zeros(k, np.uint8))
     assert np.all(none["y"] == 0)
+
+
+# ---------------------------------------------------------------------------
+# The neighbours: RMSNorm producing X, and the residual around the MLP
+# ---------------------------------------------------------------------------
+
+def test_rmsnorm_golden_example():
+    rec = {l[0]: l[1:] for l in _golden_lines("rmsnorm_worked_example.txt")}
+    h = np.array([float(v) for v in rec["h"]], dtype=np.float32)
+    w = np.array([float(v) for v in rec["w"]], dtype=np.float32)
+    x0 = oracle.rmsnorm_fp16(h, w, 0.0)[0]
+    assert [int(v) for v in x0] == [int(v, 16) for v in rec["eps0"]]
+    x1 = oracle.rmsnorm_fp16(h, w, 3.75)[0]
+    assert int(x1[0]) == int(rec["eps3.75"][0], 16)
+
+
+def test_rmsnorm_scale_invariance_and_unit_rms():
+    rng = np.random.default_rng(21)
+    h = rng.standard_normal((3, 256)).astype(np.float32)
+    w = rng.standard_normal(256).astype(np.float32)
+    x = oracle.rmsnorm_fp16(h, w, 0.0)
+    for e in (-6, 3, 20):  # power-of-two scaling is exact, so x is unchanged
+        assert np.array_equal(oracle.rmsnorm_fp16(h * np.float32(2.0 ** e), w, 0.0), x)
+    signs = np.where(rng.random((2, 64)) < 0.5, -1.0, 1.0).astype(np.float32)  # mean square exactly 1
+    wv = rng.standard_normal(64).astype(np.float32)
+    assert np.array_equal(oracle.rmsnorm_fp16(signs, wv, 0.0), (signs * wv).astype(np.float16).view(np.uint16))
+
+
+def test_rmsnorm_sign_is_the_xor_of_the_operand_signs():
+    """The predictor reads only the sign of x, which is the XOR of the signs
+    of h and w (zeros included), whatever the rounding."""
+    rng = np.random.default_rng(22)
+    h = rng.standard_normal((4, 512)).astype(np.float32)
+    w = rng.standard_normal(512).astype(np.float32)
+    h[:, :8] = 0.0
+    h[:, 8:16] = -0.0
+    h[:, 16:24] *= np.float32(1e-30)  # underflows to a signed zero in fp16
+    x = oracle.rmsnorm_fp16(h, w, 1e-6)
+    want = np.signbit(h) ^ np.signbit(w)[None, :]
+    assert np.array_equal(oracle.sign_bits(x).astype(bool), want)
+
+
+def test_mlp_block_adds_the_residual():
+    rng = np.random.default_rng(23)
+    k, d = 48, 64
+    wg = _random_bits(rng, (k, d), special=False)
+    wu = _random_bits(rng, (k, d), special=False)
+    wd = _random_bits(rng, (d, k), special=False)
+    h = rng.standard_normal((2, d)).astype(np.float32)
+    wn = rng.standard_normal(d).astype(np.float32)
+    packed = oracle.pack_signs(wg)
+    out = oracle.mlp_block(h, wn, 1e-5, packed, wg, wu, wd, 1.0)
+    x = oracle.rmsnorm_fp16(h, wn, 1e-5)
+    mask = oracle.predict_rows(packed, x, 1.0)[0]
+    assert np.array_equal(out["mask"], mask) and np.array_equal(out["x"], x)
+    m = oracle.sparse_mlp(wg, wu, wd, x, mask)["y"]
+    assert np.array_equal(out["mlp_y"], m) and np.array_equal(out["y"], h.astype(np.float64) + m)
+    zero_down = np.zeros((d, k), np.uint16)
+    assert np.array_equal(oracle.mlp_block(h, wn, 1e-5, packed, wg, wu, zero_down, 1.0)["y"], h.astype(np.float64))
+    relu = oracle.mlp_block(h, wn, 1e-5, packed, wg, None, wd, 1.0)
+    assert np.array_equal(relu["mlp_y"], oracle.relu_mlp(wg, wd, x, mask)["y"])
