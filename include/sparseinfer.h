@@ -46,7 +46,9 @@ typedef enum {
   SI_ERR_ALPHA = 4,     /* alpha is NaN or negative                        */
   SI_ERR_WORKSPACE = 5, /* workspace smaller than si_workspace_bytes()     */
   SI_ERR_HIP = 6,       /* the HIP runtime reported an error               */
-  SI_ERR_FLAGS = 7      /* unknown bits in `flags`                         */
+  SI_ERR_FLAGS = 7,     /* unknown bits in `flags`                         */
+  SI_ERR_ARG = 8        /* another argument out of range (eps, overlapping
+                           buffers)                                        */
 } si_status;
 
 /* Flags of si_sparse_mlp / si_predict_sparse_mlp. */
@@ -200,6 +202,28 @@ si_status si_predict_sparse_relu_mlp(const uint32_t* signs, const uint16_t* w_fc
                                      int d, const uint16_t* x, int b, float alpha, uint8_t* mask,
                                      int32_t* active_idx, int32_t* n_active, float* y, void* workspace,
                                      size_t workspace_bytes, uint32_t flags, int32_t* counters, void* stream);
+
+/*
+ * The MLP half of a decoder layer in one launch, with the path's neighbours
+ * fused: the RMSNorm that produces the MLP input (whose sign words the
+ * predictor needs, Section IV-B 1) and the residual add after the
+ * down-projection.  Per token t:
+ *   x_t = fp16( h_t / sqrt(mean_j(h_t,j^2) + eps) * norm_w )  (in the kernel)
+ *   y_t = h_t + MLP(x_t)   with MLP as in si_predict_sparse_mlp (gated), or
+ *                          si_predict_sparse_relu_mlp when w_up is NULL.
+ *   h      : [b][d] float32, the residual stream, read.
+ *   norm_w : [d] float32, the RMSNorm weight, read.
+ *   eps    : finite, >= 0.
+ *   y      : [b][d] float32, overwritten; must not overlap h.
+ * Other arguments, outputs and errors as si_predict_sparse_mlp.  Runs only
+ * where the single-launch path applies (si_single_launch(k, d, b) == 1);
+ * other shapes return SI_ERR_SHAPE.
+ */
+si_status si_rmsnorm_predict_sparse_mlp(const float* h, const float* norm_w, float eps, const uint32_t* signs,
+                                        const uint16_t* w_gate, const uint16_t* w_up, const uint16_t* w_down_t,
+                                        int k, int d, int b, float alpha, uint8_t* mask, int32_t* active_idx,
+                                        int32_t* n_active, float* y, void* workspace, size_t workspace_bytes,
+                                        uint32_t flags, int32_t* counters, void* stream);
 
 #ifdef __cplusplus
 }

@@ -19,7 +19,7 @@ from ._lib import SI_NO_AS, SI_NO_SPECULATION, SparseInferError
 __all__ = [
     "SI_NO_AS", "SI_NO_SPECULATION", "SparseInferError", "signs_bytes", "alpha_threshold", "workspace_bytes",
     "new_workspace", "pack_signs", "signs_to_canonical", "transpose_down", "predict",
-    "sparse_mlp", "predict_sparse_mlp", "MLPLayer",
+    "sparse_mlp", "predict_sparse_mlp", "mlp_block", "MLPLayer",
 ]
 
 
@@ -175,6 +175,37 @@ def predict_sparse_mlp(signs, w_gate, w_up, w_down_t, x, alpha, workspace, flags
     return (y, (mask, idx, n, cnt)) if outputs else y
 
 
+def mlp_block(h, norm_w, eps, signs, w_gate, w_up, w_down_t, alpha, workspace, flags: int = 0,
+              outputs: bool = False, y: torch.Tensor = None):
+    """The MLP half of a decoder layer with its neighbours fused
+    (``si_rmsnorm_predict_sparse_mlp``): ``y = h + MLP(fp16(RMSNorm(h) *
+    norm_w))``; ``h`` ``[b][d]`` and ``norm_w`` ``[d]`` float32.  Returns
+    ``y`` (and ``(mask, active_idx, n_active, counters)`` with ``outputs``);
+    ``w_up=None``: the non-gated ReLU MLP."""
+    _dev(h, "h", (torch.float32,))
+    _dev(norm_w, "norm_w", (torch.float32,), 1)
+    k, d = w_gate.shape
+    h2 = h.view(-1, d)
+    b = h2.shape[0]
+    if y is None:
+        y = torch.empty(b, d, dtype=torch.float32, device=h.device)
+    else:
+        _dev(y, "y", (torch.float32,))
+        if y.numel() != b * d:
+            raise ValueError(f"y must hold [{b}][{d}] floats")
+    if outputs:
+        mask = torch.empty(k, dtype=torch.uint8, device=h.device)
+        idx = torch.empty(k, dtype=torch.int32, device=h.device)
+        n = torch.empty(1, dtype=torch.int32, device=h.device)
+        cnt = torch.zeros(3, dtype=torch.int32, device=h.device)
+    else:
+        mask = idx = n = cnt = None
+    _lib.call("si_rmsnorm_predict_sparse_mlp", _vp(h2), _vp(norm_w), float(eps), _vp(signs), _vp(w_gate),
+              _vp(w_up), _vp(w_down_t), k, d, b, float(alpha), _vp(mask), _vp(idx), _vp(n), _vp(y),
+              _vp(workspace), workspace.numel(), flags, _vp(cnt), _stream())
+    return (y, (mask, idx, n, cnt)) if outputs else y
+
+
 class MLPLayer:
     """One layer's device-resident state: weights, packed signs and
     ``W_down^T`` (both made once at load), plus a workspace.  With
@@ -194,6 +225,12 @@ class MLPLayer:
     def __call__(self, x, alpha: float, flags: int = 0, outputs: bool = False, y: torch.Tensor = None):
         return predict_sparse_mlp(self.signs, self.w_gate, self.w_up, self.w_down_t, x, alpha, self.workspace,
                                   flags=flags, outputs=outputs, y=y)
+
+    def block(self, h, norm_w, eps: float, alpha: float, flags: int = 0, outputs: bool = False,
+              y: torch.Tensor = None):
+        """``h + MLP(RMSNorm(h) * norm_w)`` in one launch (see ``mlp_block``)."""
+        return mlp_block(h, norm_w, eps, self.signs, self.w_gate, self.w_up, self.w_down_t, alpha, self.workspace,
+                         flags=flags, outputs=outputs, y=y)
 
     def predict(self, x, alpha: float):
         return predict(self.signs, x, alpha, self.k, self.workspace)

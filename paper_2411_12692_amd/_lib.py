@@ -20,6 +20,7 @@ SI_ERR_ALPHA = 4
 SI_ERR_WORKSPACE = 5
 SI_ERR_HIP = 6
 SI_ERR_FLAGS = 7
+SI_ERR_ARG = 8
 SI_NO_AS = 1
 SI_NO_SPECULATION = 2
 
@@ -47,6 +48,8 @@ SIGNATURES = {
     "si_sparse_relu_mlp": (_i, [_p, _p, _i, _i, _p, _i, _p, _p, _p, _p, _p, _sz, _u32, _p, _p]),
     "si_predict_sparse_relu_mlp": (_i, [_p, _p, _p, _i, _i, _p, _i, _f, _p, _p, _p, _p, _p, _sz, _u32,
                                         _p, _p]),
+    "si_rmsnorm_predict_sparse_mlp": (_i, [_p, _p, _f, _p, _p, _p, _p, _i, _i, _i, _f, _p, _p, _p, _p, _p, _sz,
+                                           _u32, _p, _p]),
 }
 
 _lib = None

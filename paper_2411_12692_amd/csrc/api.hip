@@ -330,4 +330,61 @@ si_status si_predict_sparse_relu_mlp(const uint32_t* signs, const uint16_t* w_fc
                                  y, workspace, workspace_bytes, flags, counters, stream);
 }
 
+si_status si_rmsnorm_predict_sparse_mlp(const float* h, const float* norm_w, float eps, const uint32_t* signs,
+                                        const uint16_t* w_gate, const uint16_t* w_up, const uint16_t* w_down_t,
+                                        int k, int d, int b, float alpha, uint8_t* mask, int32_t* active_idx,
+                                        int32_t* n_active, float* y, void* workspace, size_t workspace_bytes,
+                                        uint32_t flags, int32_t* counters, void* stream) {
+  REQUIRE_PTR(h);
+  REQUIRE_PTR(norm_w);
+  REQUIRE_PTR(signs);
+  REQUIRE_PTR(w_gate);
+  REQUIRE_PTR(w_down_t);
+  REQUIRE_PTR(y);
+  REQUIRE_ALIGNED(h);
+  REQUIRE_ALIGNED(norm_w);
+  REQUIRE_ALIGNED(signs);
+  REQUIRE_ALIGNED(w_gate);
+  REQUIRE_ALIGNED(w_up);
+  REQUIRE_ALIGNED(w_down_t);
+  REQUIRE_ALIGNED(y);
+  REQUIRE_ALIGNED(mask);
+  REQUIRE_ALIGNED(active_idx);
+  REQUIRE_ALIGNED(n_active);
+  REQUIRE_ALIGNED(counters);
+  if (flags & ~(SI_NO_AS | SI_NO_SPECULATION)) return fail(SI_ERR_FLAGS, "unknown flags 0x%x", flags);
+  if (si_status s = check_kd(k, d)) return s;
+  if (si_status s = check_b(b)) return s;
+  if (std::isnan(alpha) || alpha < 0.0f) return fail(SI_ERR_ALPHA, "alpha=%g must be >= 0 (or +inf)", (double)alpha);
+  if (!std::isfinite(eps) || eps < 0.0f) return fail(SI_ERR_ARG, "eps=%g must be finite and >= 0", (double)eps);
+  const uintptr_t ha = reinterpret_cast<uintptr_t>(h), ya = reinterpret_cast<uintptr_t>(y);
+  const uintptr_t nb = (uintptr_t)b * (uintptr_t)d * sizeof(float);
+  if (ha < ya + nb && ya < ha + nb) return fail(SI_ERR_ARG, "h and y overlap");
+  if (si_status s = check_ws(workspace, workspace_bytes, k, b)) return s;
+  if (!si::owned_supported(k, d, b))
+    return fail(SI_ERR_SHAPE, "k=%d d=%d b=%d: the decoder-block call needs the single-launch path", k, d, b);
+  char* base = static_cast<char*>(workspace);
+  si::LayerCall c;
+  c.signs = signs;
+  c.w_gate = w_gate;
+  c.w_up = w_up;
+  c.w_down_t = w_down_t;
+  c.k = k;
+  c.d = d;
+  c.b = b;
+  c.T = si_alpha_threshold(alpha, d);
+  c.margin = d / 16;
+  c.flags = flags;
+  c.mask = mask;
+  c.idx = active_idx;
+  c.n_out = n_active ? n_active : reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;
+  c.y = y;
+  c.ws = workspace;
+  c.counters = counters;
+  c.h = h;
+  c.norm_w = norm_w;
+  c.eps = eps;
+  return hip_status(si::launch_owned(c, (hipStream_t)stream), "decoder-block launch");
+}
+
 }  // extern "C"

@@ -74,6 +74,7 @@ constexpr int kOW = 8;
 constexpr int kOT = kOW * kWave;
 constexpr int kOSignUnits = (kMaxD / 128 + kOW - 1) / kOW;  // sign units per wave and pass, at most (8)
 constexpr int kFin = kOW - 1;      // the wave that finishes the prediction
+constexpr int kTileWave = kOW - 2; // the wave that initialises the owner's tile of y
 constexpr int kODN = 8;            // W_down^T pieces per wave and down round
 constexpr int kODownRound = kOW * kODN;
 static_assert(kODN * kMaxB <= kWave, "a wave polls the h3 words of its pieces, one lane per (piece, token)");
@@ -99,6 +100,9 @@ struct OwnedArgs {
   uint64_t* zflag;         // [tiles] tag once the tile of y is zero
   int32_t* counts;         // [blocks][2] W_up rows read, W_down^T rows read (tile-0 items)
   float* y;
+  const float* h;          // decoder-block mode: the residual stream [b][d] (x = RMSNorm(h) * norm_w)
+  const float* norm_w;     // [d]
+  float eps;
 };
 
 template <int BM, int NU>
@@ -120,6 +124,7 @@ struct OwnedLds {
   uint32_t pm[4 * kMaxPairs];  // the group's published mask words
   uint32_t srow[kMaxOwnRows];  // conf << 31 | row of the block's kept rows, ascending
   int wsum[kOW];
+  float nsum[kOW][kMaxB];  // decoder-block mode: per-wave sums of squares of the tokens
   int n_own, n_up, n_down;
   uint32_t epoch;
 };
@@ -269,18 +274,20 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     if (predict) load_signs(0);
     else if (wv == kFin) mbyte = a.mask_in[r0 + min(lane, Rb - 1)];
   }
-  // the owner of tile blk of y zeroes it (the finishing wave, which later
-  // announces it in the tile's flag)
-  if (owns_tile && wv == kFin) {
+  // the owner of tile blk of y zeroes it (in decoder-block mode it copies
+  // the residual in later); the same wave later announces it in the tile's
+  // flag
+  const bool block_mode = a.h != nullptr;
+  if (owns_tile && !block_mode && wv == kTileWave) {
     const int half_cols = min(kTile, d - blk * kTile) / 2;
     for (int t = 0; t < b; ++t) {
       uint64_t* yt = reinterpret_cast<uint64_t*>(a.y + (size_t)t * d + blk * kTile);
       for (int c = lane; c < half_cols; c += kWave) st_agent64(yt + c, 0ull);
     }
   }
-  {
-    // token t's unit u at xs[t * XS + u] (XS = NU * 64 >= U)
-    constexpr int XS = OwnedLds<BM, NU>::kUnits;
+  // token t's unit u at xs[t * XS + u] (XS = NU * 64 >= U)
+  constexpr int XS = OwnedLds<BM, NU>::kUnits;
+  if (!block_mode) {
     const u32x4* xg = reinterpret_cast<const u32x4*>(a.x);
     const int nx = b * U;
     for (int i = tid; i < BM * XS; i += kOT) {
@@ -293,6 +300,58 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         L.n_down = 0;
       }
       L.xs[i] = (t < b && u < U) ? xv : u32x4{0, 0, 0, 0};
+    }
+  } else {
+    // decoder-block mode: x = RMSNorm(h) * norm_w in fp16, formed here from
+    // the fp32 residual stream (sums of squares over the block, then every
+    // unit of 8 values scaled and rounded)
+    const float4* hg = reinterpret_cast<const float4*>(a.h);
+    const float4* wg4 = reinterpret_cast<const float4*>(a.norm_w);
+    float ss[BM];
+#pragma unroll
+    for (int t = 0; t < BM; ++t) ss[t] = 0.f;
+    for (int i = tid; i < b * U; i += kOT) {
+      const int t = i / U;
+      const float4 p = hg[2 * i], q = hg[2 * i + 1];
+      const float v = p.x * p.x + p.y * p.y + p.z * p.z + p.w * p.w + q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
+#pragma unroll
+      for (int tt = 0; tt < BM; ++tt) ss[tt] += tt == t ? v : 0.f;
+    }
+    if (tid == 0) {
+      asm volatile("" ::: "memory");
+      L.epoch = ld_agent(&a.hdr[H_EPOCH]);
+      L.n_up = 0;
+      L.n_down = 0;
+    }
+#pragma unroll
+    for (int t = 0; t < BM; ++t) {
+      const float v = wave_sum(ss[t]);
+      if (lane == 0) L.nsum[wv][t] = v;
+    }
+    __syncthreads();
+    float r[BM];
+#pragma unroll
+    for (int t = 0; t < BM; ++t) {
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < kOW; ++w) v += L.nsum[w][t];
+      r[t] = 1.0f / sqrtf(v / (float)d + a.eps);
+    }
+    for (int i = tid; i < BM * XS; i += kOT) {
+      const int t = i / XS, u = i - t * XS;
+      u32x4 xv{0, 0, 0, 0};
+      if (t < b && u < U) {
+        float rt = 0.f;
+#pragma unroll
+        for (int tt = 0; tt < BM; ++tt) rt = tt == t ? r[tt] : rt;
+        const float4 p = hg[2 * (t * U + u)], q = hg[2 * (t * U + u) + 1];
+        const float4 wp = wg4[2 * u], wq = wg4[2 * u + 1];
+        xv.x = pack_h2((p.x * rt) * wp.x, (p.y * rt) * wp.y);
+        xv.y = pack_h2((p.z * rt) * wp.z, (p.w * rt) * wp.w);
+        xv.z = pack_h2((q.x * rt) * wq.x, (q.y * rt) * wq.y);
+        xv.w = pack_h2((q.z * rt) * wq.z, (q.w * rt) * wq.w);
+      }
+      L.xs[i] = xv;
     }
   }
   __syncthreads();
@@ -384,6 +443,16 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
     if (predict && any_rows && s + 1 < nsub) __syncthreads();  // the partial counts are reused
   }
+  // decoder-block mode: the owner's tile of y starts as the residual h
+  // (while the finishing wave publishes)
+  if (owns_tile && block_mode && wv == kTileWave) {
+    const int half_cols = min(kTile, d - blk * kTile) / 2;
+    for (int t = 0; t < b; ++t) {
+      const uint64_t* ht = reinterpret_cast<const uint64_t*>(a.h + (size_t)t * d + blk * kTile);
+      uint64_t* yt = reinterpret_cast<uint64_t*>(a.y + (size_t)t * d + blk * kTile);
+      for (int c = lane; c < half_cols; c += kWave) st_agent64(yt + c, ht[c]);
+    }
+  }
   __syncthreads();
   n_own = uniform(L.n_own);
   SI_TRACE_MARK(3);
@@ -423,7 +492,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       advance_epoch(a.hdr, epoch);
     }
     census_done = true;
-    if (owns_tile && wv == kFin) {  // the tile's zeroing stores have landed by now
+    if (owns_tile && wv == kTileWave) {  // the tile's first stores have landed by now
       wait_own_stores();
       if (lane == 0) st_agent64(&a.zflag[blk], tagged(tag, 1u));
     }
@@ -707,6 +776,9 @@ static hipError_t owned_b(const LayerCall& c, hipStream_t s) {
     a.zflag = reinterpret_cast<uint64_t*>(base + L.zflag);
     a.counts = reinterpret_cast<int32_t*>(base + L.counts);
     a.y = c.y;
+    a.h = c.h;
+    a.norm_w = c.norm_w;
+    a.eps = c.eps;
     k_owned<BM, NU><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !c.counters || !c.y) return e;

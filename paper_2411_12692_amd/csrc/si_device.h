@@ -88,6 +88,16 @@ __device__ inline uint32_t sign_word(const u32x4* p) {
 
 __device__ inline f16x2 as_h2(uint32_t v) { return __builtin_bit_cast(f16x2, v); }
 
+// Two floats rounded to fp16 (to nearest even), low half first.  The
+// values are pinned as they are first: the compiler would otherwise fold a
+// product that feeds the conversion into a mixed-precision FMA with a +0
+// addend, which turns a -0 product into +0 (the predictor reads that sign).
+__device__ inline uint32_t pack_h2(float lo, float hi) {
+  asm volatile("" : "+v"(lo), "+v"(hi));
+  const _Float16 a = (_Float16)lo, b = (_Float16)hi;
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+
 // acc + sum of the 8 products of two 16-byte fp16 vectors (fp32 accumulation).
 __device__ inline float dot8(u32x4 a, u32x4 b, float acc) {
   acc = __builtin_amdgcn_fdot2(as_h2(a.x), as_h2(b.x), acc, false);

@@ -50,6 +50,11 @@ struct LayerCall {
   float* y = nullptr;
   void* ws = nullptr;
   int32_t* counters = nullptr;
+  // decoder-block mode (row-owning kernel only): x = fp16(RMSNorm(h) * norm_w)
+  // is formed in the kernel (x must be NULL) and y = h + MLP(x)
+  const float* h = nullptr;
+  const float* norm_w = nullptr;
+  float eps = 0.f;
 };
 bool layer_supported(int k, int d, int b);
 hipError_t launch_layer(const LayerCall& c, hipStream_t s);
