@@ -5,7 +5,10 @@ packing, sign-bit prediction (Eq. (2)), compaction, sparse gate/up with
 actual sparsity and sparse down-projection, for the 7B-shaped layer
 (d = 4096, k = 11008) with planted sparsity s = 0.9, alpha = 1.0, batch 1.
 ``--mlp relu`` times the non-gated ReLU MLP (no W_up) of an OPT-6.7B-shaped
-layer (d = 4096, k = 16384) instead, same sparsity and alpha.
+layer (d = 4096, k = 16384) instead, same sparsity and alpha; ``--mlp block``
+times the 7B layer as a decoder-block call (RMSNorm of the fp32 residual
+stream and the residual add fused around the path) and, for comparison, the
+plain call on the same layers.
 Steps cycle through a pool of independently seeded layers whose weights
 (>= 4.4 GB) exceed the 256 MB Infinity Cache, so every step reads its bytes
 from HBM.  The timed loop is replayed from a HIP graph (the per-call host
@@ -36,11 +39,16 @@ HBM_PEAK_GBS = 8000.0
 # the non-gated workload (--mlp relu): OPT-6.7B's MLP shape
 RELU_METRIC = "µs per non-gated ReLU MLP layer (predict+sparse GEMV) at OPT-6.7B shape, s=0.9; effective HBM GB/s"
 RELU_D, RELU_K = 4096, 16384
+BLOCK_METRIC = ("µs per decoder-block MLP call (RMSNorm + predict + sparse GEMV + residual) at 7B shape, s=0.9; "
+                "effective HBM GB/s")
 
 
-def algorithmic_bytes(k, d, b, n_gate, n_up, n_down):
-    """Bytes the method itself must move for one layer and one step."""
-    return k * d // 8 + 2 * d * b + 2 * d * (n_gate + n_up + n_down) + 4 * d * b
+def algorithmic_bytes(k, d, b, n_gate, n_up, n_down, block=False):
+    """Bytes the method itself must move for one layer and one step (the
+    decoder-block call reads the fp32 residual stream and the norm weight
+    instead of the fp16 x)."""
+    x_bytes = 4 * d * b + 4 * d if block else 2 * d * b
+    return k * d // 8 + x_bytes + 2 * d * (n_gate + n_up + n_down) + 4 * d * b
 
 
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_7b_s0.9_counters.txt")
@@ -83,9 +91,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=256)
     ap.add_argument("--layers", type=int, default=16, help="size of the rotating layer pool")
     ap.add_argument("--alpha", type=float, default=1.0)
-    ap.add_argument("--mlp", choices=("gated", "relu"), default="gated",
+    ap.add_argument("--mlp", choices=("gated", "relu", "block"), default="gated",
                     help="gated: the 7B-shaped gated MLP (default); relu: the non-gated ReLU MLP of an "
-                         "OPT-6.7B-shaped layer")
+                         "OPT-6.7B-shaped layer; block: the 7B layer with RMSNorm and residual fused")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--launches", type=int, default=256, help="individually timed launches for the roofline")
@@ -95,15 +103,15 @@ def parse():
     return ap.parse_args()
 
 
-def profile_pass(layers, xs, ys, alpha, calls):
+def profile_pass(step, n_layers, calls, dev):
     """Eager launches only (counter collection serialises dispatches), then a
     plain copy of known size: 256 MiB read + 256 MiB written."""
     import torch
 
     for i in range(calls):
-        layers[i % len(layers)](xs[i % len(xs)], alpha, y=ys[i % len(ys)])
+        step(i)
     torch.cuda.synchronize()
-    src = torch.empty(128 << 20, dtype=torch.float16, device=xs[0].device).fill_(1.0)
+    src = torch.empty(128 << 20, dtype=torch.float16, device=dev).fill_(1.0)
     dst = torch.empty_like(src)
     torch.cuda.synchronize()
     for _ in range(4):
@@ -112,12 +120,12 @@ def profile_pass(layers, xs, ys, alpha, calls):
     print(f"# profile pass: {calls} layer calls, 4 copies of {src.numel() * 2} bytes", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D):
+def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None):
     """Time the CPU oracle (test infrastructure, never tuned) on a bounded
     sample of the same workload: predict + masked MLP on the first layers of
     the pool, repeated until the budget is spent, with one BLAS thread
-    (``wu is None``: the non-gated MLP)."""
-    import numpy as np
+    (``wu is None``: the non-gated MLP; ``block`` = per-layer ``(h, norm_w,
+    eps)``: the decoder-block form, RMSNorm and residual included)."""
     from threadpoolctl import threadpool_limits
 
     import oracle
@@ -125,18 +133,25 @@ def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D):
     total_bytes, total_s, calls = 0.0, 0.0, 0
     with threadpool_limits(limits=1):
         while total_s < budget_s:
-            for wg, wu, wd, x, packed in layers_host:
+            for li, (wg, wu, wd, x, packed) in enumerate(layers_host):
                 t0 = time.perf_counter()
-                mask, _, _ = oracle.predict_rows(packed, x, alpha)
-                if wu is None:
-                    out = oracle.relu_mlp(wg, wd, x, mask)
+                if block is not None:
+                    h, nw, eps = block[li]
+                    out = oracle.mlp_block(h, nw, eps, packed, wg, wu, wd, alpha)
                 else:
-                    out = oracle.sparse_mlp(wg, wu, wd, x, mask)
+                    mask, _, _ = oracle.predict_rows(packed, x, alpha)
+                    if wu is None:
+                        out = oracle.relu_mlp(wg, wd, x, mask)
+                    else:
+                        out = oracle.sparse_mlp(wg, wu, wd, x, mask)
                 total_s += time.perf_counter() - t0
                 calls += 1
-                total_bytes += algorithmic_bytes(k, d, x.shape[0], out["n_gate"], out["n_up"], out["n_down"])
+                total_bytes += algorithmic_bytes(k, d, x.shape[0], out["n_gate"], out["n_up"], out["n_down"],
+                                                 block=block is not None)
                 if total_s >= budget_s:
                     break
+    what = ("rmsnorm_fp16 + predict_rows + sparse_mlp + residual" if block is not None else
+            f"predict_rows + {'relu_mlp' if layers_host[0][1] is None else 'sparse_mlp'}")
     return {
         "value": round(total_bytes / total_s / 1e9, 3),
         "unit": "GB/s",
@@ -144,10 +159,45 @@ def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D):
         "cores": 1,
         "kind": "oracle",
         "sample": f"{calls} layer calls over the first {len(layers_host)} layers of the pool "
-                  f"(predict_rows + {'relu_mlp' if layers_host[0][1] is None else 'sparse_mlp'}, "
-                  f"numpy float64, 1 thread, {total_s:.1f} s)",
+                  f"({what}, numpy float64, 1 thread, {total_s:.1f} s)",
         "cpu": platform.processor() or platform.machine(),
     }
+
+
+def time_graph(step, n_layers, steps_wanted, warmup_wanted):
+    """Replay a HIP graph of back-to-back steps (one pass over the layer pool
+    or more) and return (us per step, steps, warm-up steps, wall us per
+    step); events on the replay stream bracket the timed replays."""
+    import torch
+
+    stream = torch.cuda.Stream()
+    per_graph = n_layers * max(1, 64 // n_layers)
+    with torch.cuda.stream(stream):
+        for i in range(per_graph):  # warm the path on the capture stream
+            step(i)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        for i in range(per_graph):
+            step(i)
+    torch.cuda.synchronize()
+    reps = max(1, math.ceil(steps_wanted / per_graph))
+    wreps = max(1, math.ceil(warmup_wanted / per_graph))
+    steps, warmup = reps * per_graph, wreps * per_graph
+    for _ in range(wreps):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(reps):
+            graph.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return e0.elapsed_time(e1) * 1e3 / steps, steps, warmup, wall * 1e6 / steps
 
 
 def main():
@@ -173,14 +223,21 @@ def main():
     si._lib.load()  # fails loudly if the library is not built
 
     relu = args.mlp == "relu"
+    block = args.mlp == "block"
     D_, K_ = (RELU_D, RELU_K) if relu else (D, K)
+    EPS = 1e-5
     L = args.layers
-    layers, xs, host = [], [], []
+    layers, xs, hs, nws, host, host_block = [], [], [], [], [], []
     for l in range(L):
         # the non-gated layer takes the planted W_gate as its W_fc1
         pl = synth.planted_layer(D_, K_, S, config=7 if relu else 2, layer=l, device=dev)
         layers.append(si.MLPLayer(pl.w_gate, None if relu else pl.w_up, pl.w_down))
         xs.append(pl.x)
+        if block:
+            # residual stream with the planted token's signs, positive norm weight
+            hs.append(pl.x.float() * 3.0)
+            g = torch.Generator(device="cpu").manual_seed(1000 + l)
+            nws.append((0.5 + torch.rand(D_, generator=g)).to(dev))
         if not args.no_cpu_baseline and l < 2:
             def u16(t):
                 return t.cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
@@ -188,58 +245,42 @@ def main():
             wu = None if relu else u16(pl.w_up)
             import oracle
             host.append((wg, wu, wd, xh, oracle.pack_signs(wg)))
+            if block:
+                host_block.append((hs[-1].cpu().numpy(), nws[-1].cpu().numpy(), EPS))
         del pl
     torch.cuda.synchronize()
     print(f"# pool of {L} layers ready", file=sys.stderr, flush=True)
 
-    # per-layer work counters (deterministic per layer) -> algorithmic bytes
     ys = [torch.empty(1, D_, dtype=torch.float32, device=dev) for _ in range(L)]
+
+    def step(i, outputs=False):
+        l = i % L
+        if block:
+            return layers[l].block(hs[l], nws[l], EPS, args.alpha, outputs=outputs, y=ys[l])
+        return layers[l](xs[l], args.alpha, outputs=outputs, y=ys[l])
+
+    # per-layer work counters (deterministic per layer) -> algorithmic bytes
     counts = []
     for l in range(L):
-        _, (_, _, _, c) = layers[l](xs[l], args.alpha, outputs=True, y=ys[l])
+        _, (_, _, _, c) = step(l, outputs=True)
         counts.append(c)
     torch.cuda.synchronize()
     counts = [c.tolist() for c in counts]
     if args.profile_pass:
-        profile_pass(layers, xs, ys, args.alpha, max(args.launches, L))
+        profile_pass(step, L, max(args.launches, L), dev)
         return
-    bytes_per_layer = [algorithmic_bytes(K_, D_, 1, *c) for c in counts]
+    bytes_per_layer = [algorithmic_bytes(K_, D_, 1, *c, block=block) for c in counts]
     mean_bytes = sum(bytes_per_layer) / L
 
-    # graph of one pass over the pool, replayed
-    stream = torch.cuda.Stream()
-    per_graph = L * max(1, 64 // L)
-    with torch.cuda.stream(stream):
-        for i in range(per_graph):  # warm the path on the capture stream
-            layers[i % L](xs[i % L], args.alpha, y=ys[i % L])
-    torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph, stream=stream):
-        for i in range(per_graph):
-            layers[i % L](xs[i % L], args.alpha, y=ys[i % L])
-    torch.cuda.synchronize()
-    reps = max(1, math.ceil(args.steps / per_graph))
-    wreps = max(1, math.ceil(args.warmup / per_graph))
-    steps, warmup = reps * per_graph, wreps * per_graph
-    for _ in range(wreps):
-        graph.replay()
-    torch.cuda.synchronize()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
-    e0.record(stream)
-    with torch.cuda.stream(stream):
-        for _ in range(reps):
-            graph.replay()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    gpu_ms = e0.elapsed_time(e1)
-    us_per_layer = gpu_ms * 1e3 / steps
-    print(f"# timed {steps} steps: {us_per_layer:.3f} us/layer (wall {wall * 1e6 / steps:.3f})",
-          file=sys.stderr, flush=True)
+    us_per_layer, steps, warmup, wall_us = time_graph(step, L, args.steps, args.warmup)
+    print(f"# timed {steps} steps: {us_per_layer:.3f} us/layer (wall {wall_us:.3f})", file=sys.stderr, flush=True)
+    plain_us = None
+    if block:  # the same layers through the plain call (x given, no residual), for comparison
+        plain_us, _, _, _ = time_graph(lambda i: layers[i % L](xs[i % L], args.alpha, y=ys[i % L]), L,
+                                       args.steps, args.warmup)
+        print(f"# plain call on the same layers: {plain_us:.3f} us/layer", file=sys.stderr, flush=True)
 
-    # The timed graph holds nothing but k_owned launches on `stream`, so the
+    # The timed graph holds nothing but k_owned launches on one stream, so the
     # per-step time above is that kernel's average launch duration.
     achieved = mean_bytes / us_per_layer / 1e3
 
@@ -247,18 +288,19 @@ def main():
     # queued behind a spin kernel so that host enqueue time stays out).
     M = args.launches
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(M)]
+    stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
         torch.cuda._sleep(int(2.4e9 * 0.02 * max(1, M / 256)))
         for i in range(M):
             a, b = evs[i]
             a.record(stream)
-            layers[i % L](xs[i % L], args.alpha, y=ys[i % L])
+            step(i)
             b.record(stream)
     torch.cuda.synchronize()
     isolated_us = sum(a.elapsed_time(b) * 1e3 for a, b in evs) / M
 
     result = {
-        "metric": RELU_METRIC if relu else METRIC,
+        "metric": RELU_METRIC if relu else BLOCK_METRIC if block else METRIC,
         "value": round(mean_bytes / us_per_layer / 1e3, 2),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -274,6 +316,8 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": (f"OPT-6.7B-shaped non-gated ReLU MLP layer (no W_up) d={D_} k={K_}" if relu else
+                         f"7B-shaped ReLU gated MLP layer d={D_} k={K_} as a decoder-block call (RMSNorm of the "
+                         f"fp32 residual stream, eps={EPS}, and the residual add fused)" if block else
                          f"7B-shaped ReLU gated MLP layer d={D_} k={K_}") +
                         f", planted sparsity s={S}, alpha={args.alpha}, batch 1, rotating pool of {L} layers, "
                         f"HIP-graph replay",
@@ -288,13 +332,16 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(RELU_COUNTERS_FILE if relu else COUNTERS_FILE),
+            "traffic": None if block else measured_traffic(RELU_COUNTERS_FILE if relu else COUNTERS_FILE),
             "launch_us": round(us_per_layer, 3),
             "isolated_launch_us": round(isolated_us, 3),
         },
     }
+    if plain_us is not None:
+        result["plain_call_us"] = round(plain_us, 3)
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(host, args.alpha, args.cpu_seconds, K_, D_)
+        result["cpu_baseline"] = cpu_baseline(host, args.alpha, args.cpu_seconds, K_, D_,
+                                              block=host_block if block else None)
     print(json.dumps(result), flush=True)
 
 

@@ -287,6 +287,55 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   }
   // token t's unit u at xs[t * XS + u] (XS = NU * 64 >= U)
   constexpr int XS = OwnedLds<BM, NU>::kUnits;
+  // decoder-block mode: h and norm_w as 16-byte vectors; each thread's
+  // units (two at most) are kept in registers from the sums of squares to
+  // the scaling, which runs once the counts are done
+  const float4* hg = reinterpret_cast<const float4*>(a.h);
+  const float4* wg4 = reinterpret_cast<const float4*>(a.norm_w);
+  constexpr int J = (BM * XS + kOT - 1) / kOT;  // units per thread (incl. padding)
+  constexpr bool kKeep = J <= 2;
+  float4 hr[kKeep ? J : 1][2], wr[kKeep ? J : 1][2];
+  // decoder-block mode: x = the fp16 rounding of h * r_t * norm_w, r_t the
+  // token's RMS normaliser from the block's sums of squares
+  auto scale_x = [&]() {
+    float r[BM];
+#pragma unroll
+    for (int t = 0; t < BM; ++t) {
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < kOW; ++w) v += L.nsum[w][t];
+      r[t] = 1.0f / sqrtf(v / (float)d + a.eps);
+    }
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const int i = tid + j * kOT, t = i / XS, u = i - t * XS;
+      if (i < BM * XS) {
+        u32x4 xv{0, 0, 0, 0};
+        if (t < b && u < U) {
+          float rt = 0.f;
+#pragma unroll
+          for (int tt = 0; tt < BM; ++tt) rt = tt == t ? r[tt] : rt;
+          float4 p, q, wp, wq;
+          if constexpr (kKeep) {
+            p = hr[j][0];
+            q = hr[j][1];
+            wp = wr[j][0];
+            wq = wr[j][1];
+          } else {
+            p = hg[2 * (t * U + u)];
+            q = hg[2 * (t * U + u) + 1];
+            wp = wg4[2 * u];
+            wq = wg4[2 * u + 1];
+          }
+          xv.x = pack_h2((p.x * rt) * wp.x, (p.y * rt) * wp.y);
+          xv.y = pack_h2((p.z * rt) * wp.z, (p.w * rt) * wp.w);
+          xv.z = pack_h2((q.x * rt) * wq.x, (q.y * rt) * wq.y);
+          xv.w = pack_h2((q.z * rt) * wq.z, (q.w * rt) * wq.w);
+        }
+        L.xs[i] = xv;
+      }
+    }
+  };
   if (!block_mode) {
     const u32x4* xg = reinterpret_cast<const u32x4*>(a.x);
     const int nx = b * U;
@@ -303,19 +352,44 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
   } else {
     // decoder-block mode: x = RMSNorm(h) * norm_w in fp16, formed here from
-    // the fp32 residual stream (sums of squares over the block, then every
-    // unit of 8 values scaled and rounded)
-    const float4* hg = reinterpret_cast<const float4*>(a.h);
-    const float4* wg4 = reinterpret_cast<const float4*>(a.norm_w);
+    // the fp32 residual stream: the sums of squares over the block, then
+    // every unit of 8 values scaled and rounded.  Where a thread has at most
+    // two units (b * d <= 8192) its h and norm_w values stay in registers
+    // between the two steps; otherwise they are read again.
     float ss[BM];
 #pragma unroll
     for (int t = 0; t < BM; ++t) ss[t] = 0.f;
-    for (int i = tid; i < b * U; i += kOT) {
-      const int t = i / U;
-      const float4 p = hg[2 * i], q = hg[2 * i + 1];
-      const float v = p.x * p.x + p.y * p.y + p.z * p.z + p.w * p.w + q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
 #pragma unroll
-      for (int tt = 0; tt < BM; ++tt) ss[tt] += tt == t ? v : 0.f;
+    for (int j = 0; j < J; ++j) {
+      const int i = tid + j * kOT, t = i / XS, u = i - t * XS;
+      if (i < BM * XS && t < b && u < U) {
+        const float4 p = hg[2 * (t * U + u)], q = hg[2 * (t * U + u) + 1];
+        if constexpr (kKeep) {
+          hr[j][0] = p;
+          hr[j][1] = q;
+        }
+        const float v = p.x * p.x + p.y * p.y + p.z * p.z + p.w * p.w + q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
+#pragma unroll
+        for (int tt = 0; tt < BM; ++tt) ss[tt] += tt == t ? v : 0.f;
+        // the signs of this unit of x need no norm: each is the XOR of the
+        // signs of h and norm_w (the scale is positive, and rounding to
+        // fp16 keeps the sign, zeros included), so the predictor's sign
+        // byte is written now (byte u of the token's sign words)
+        const float4 wp = wg4[2 * u], wq = wg4[2 * u + 1];
+        if constexpr (kKeep) {
+          wr[j][0] = wp;
+          wr[j][1] = wq;
+        }
+        const uint32_t hb = (__float_as_uint(p.x) >> 31) | ((__float_as_uint(p.y) >> 31) << 1) |
+                            ((__float_as_uint(p.z) >> 31) << 2) | ((__float_as_uint(p.w) >> 31) << 3) |
+                            ((__float_as_uint(q.x) >> 31) << 4) | ((__float_as_uint(q.y) >> 31) << 5) |
+                            ((__float_as_uint(q.z) >> 31) << 6) | ((__float_as_uint(q.w) >> 31) << 7);
+        const uint32_t wb = (__float_as_uint(wp.x) >> 31) | ((__float_as_uint(wp.y) >> 31) << 1) |
+                            ((__float_as_uint(wp.z) >> 31) << 2) | ((__float_as_uint(wp.w) >> 31) << 3) |
+                            ((__float_as_uint(wq.x) >> 31) << 4) | ((__float_as_uint(wq.y) >> 31) << 5) |
+                            ((__float_as_uint(wq.z) >> 31) << 6) | ((__float_as_uint(wq.w) >> 31) << 7);
+        reinterpret_cast<uint8_t*>(L.xw)[t * 4 * W + u] = (uint8_t)(hb ^ wb);
+      }
     }
     if (tid == 0) {
       asm volatile("" ::: "memory");
@@ -325,43 +399,21 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
 #pragma unroll
     for (int t = 0; t < BM; ++t) {
-      const float v = wave_sum(ss[t]);
+      const float v = wave_total(ss[t]);
       if (lane == 0) L.nsum[wv][t] = v;
-    }
-    __syncthreads();
-    float r[BM];
-#pragma unroll
-    for (int t = 0; t < BM; ++t) {
-      float v = 0.f;
-#pragma unroll
-      for (int w = 0; w < kOW; ++w) v += L.nsum[w][t];
-      r[t] = 1.0f / sqrtf(v / (float)d + a.eps);
-    }
-    for (int i = tid; i < BM * XS; i += kOT) {
-      const int t = i / XS, u = i - t * XS;
-      u32x4 xv{0, 0, 0, 0};
-      if (t < b && u < U) {
-        float rt = 0.f;
-#pragma unroll
-        for (int tt = 0; tt < BM; ++tt) rt = tt == t ? r[tt] : rt;
-        const float4 p = hg[2 * (t * U + u)], q = hg[2 * (t * U + u) + 1];
-        const float4 wp = wg4[2 * u], wq = wg4[2 * u + 1];
-        xv.x = pack_h2((p.x * rt) * wp.x, (p.y * rt) * wp.y);
-        xv.y = pack_h2((p.z * rt) * wp.z, (p.w * rt) * wp.w);
-        xv.z = pack_h2((q.x * rt) * wq.x, (q.y * rt) * wq.y);
-        xv.w = pack_h2((q.z * rt) * wq.z, (q.w * rt) * wq.w);
-      }
-      L.xs[i] = xv;
     }
   }
   __syncthreads();
+  if constexpr (!kKeep) {  // h and norm_w are read again: before the counts, not behind the publishing stores
+    if (block_mode) scale_x();
+  }
   const uint32_t epoch = uniform(L.epoch);
   const uint32_t tag = epoch_tag(epoch);
   // consumed here, where the wait for it is covered by the token requests (a
   // load left outstanding into the loop below would make the compiler wait
   // for every outstanding request, stores included, inside it)
   bool mkeep = mbyte != 0;
-  if (predict) {
+  if (predict && !block_mode) {  // (written with the norm in decoder-block mode)
     for (int i = tid; i < BM * W; i += kOT) {  // tokens b..BM-1 are zero
       const int t = i / W, w = i - t * W;
       L.xw[i] = sign_word(&L.xs[t * OwnedLds<BM, NU>::kUnits + 4 * w]);
@@ -443,14 +495,19 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
     if (predict && any_rows && s + 1 < nsub) __syncthreads();  // the partial counts are reused
   }
-  // decoder-block mode: the owner's tile of y starts as the residual h
-  // (while the finishing wave publishes)
-  if (owns_tile && block_mode && wv == kTileWave) {
-    const int half_cols = min(kTile, d - blk * kTile) / 2;
-    for (int t = 0; t < b; ++t) {
-      const uint64_t* ht = reinterpret_cast<const uint64_t*>(a.h + (size_t)t * d + blk * kTile);
-      uint64_t* yt = reinterpret_cast<uint64_t*>(a.y + (size_t)t * d + blk * kTile);
-      for (int c = lane; c < half_cols; c += kWave) st_agent64(yt + c, ht[c]);
+  // decoder-block mode: x itself (for the gate/up products, needed only
+  // after the group exchange) is scaled and rounded now from the registers,
+  // and the owner's tile of y starts as the residual h (while the finishing
+  // wave publishes)
+  if (block_mode) {
+    if constexpr (kKeep) scale_x();
+    if (owns_tile && wv == kTileWave) {
+      const int half_cols = min(kTile, d - blk * kTile) / 2;
+      for (int t = 0; t < b; ++t) {
+        const uint64_t* ht = reinterpret_cast<const uint64_t*>(a.h + (size_t)t * d + blk * kTile);
+        uint64_t* yt = reinterpret_cast<uint64_t*>(a.y + (size_t)t * d + blk * kTile);
+        for (int c = lane; c < half_cols; c += kWave) st_agent64(yt + c, ht[c]);
+      }
     }
   }
   __syncthreads();
