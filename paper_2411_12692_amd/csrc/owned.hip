@@ -228,7 +228,10 @@ __device__ inline void row_dots2(const u32x4 (&v)[NU], const u32x4 (&w)[NU], con
   }
 }
 
-template <int BM, int NU>
+// BLOCK: the decoder-block form (x from the RMSNorm of h, y = h + MLP),
+// a separate instance so that the plain form carries none of its code (its
+// presence alone cost the plain form 0.3 us per call)
+template <int BM, int NU, bool BLOCK>
 __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
   OwnedLds<BM, NU>& L = *reinterpret_cast<OwnedLds<BM, NU>*>(lds_raw);
@@ -277,8 +280,8 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   // the owner of tile blk of y zeroes it (in decoder-block mode it copies
   // the residual in later); the same wave later announces it in the tile's
   // flag
-  const bool block_mode = a.h != nullptr;
-  if (owns_tile && !block_mode && wv == kTileWave) {
+  constexpr bool block_mode = BLOCK;
+  if (!block_mode && owns_tile && wv == kTileWave) {
     const int half_cols = min(kTile, d - blk * kTile) / 2;
     for (int t = 0; t < b; ++t) {
       uint64_t* yt = reinterpret_cast<uint64_t*>(a.y + (size_t)t * d + blk * kTile);
@@ -336,7 +339,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       }
     }
   };
-  if (!block_mode) {
+  if constexpr (!block_mode) {
     const u32x4* xg = reinterpret_cast<const u32x4*>(a.x);
     const int nx = b * U;
     for (int i = tid; i < BM * XS; i += kOT) {
@@ -404,22 +407,22 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
   }
   __syncthreads();
-  if constexpr (!kKeep) {  // h and norm_w are read again: before the counts, not behind the publishing stores
-    if (block_mode) scale_x();
-  }
+  if constexpr (block_mode && !kKeep) scale_x();  // h and norm_w read again: before the counts, not behind the publishing stores
   const uint32_t epoch = uniform(L.epoch);
   const uint32_t tag = epoch_tag(epoch);
   // consumed here, where the wait for it is covered by the token requests (a
   // load left outstanding into the loop below would make the compiler wait
   // for every outstanding request, stores included, inside it)
   bool mkeep = mbyte != 0;
-  if (predict && !block_mode) {  // (written with the norm in decoder-block mode)
-    for (int i = tid; i < BM * W; i += kOT) {  // tokens b..BM-1 are zero
-      const int t = i / W, w = i - t * W;
-      L.xw[i] = sign_word(&L.xs[t * OwnedLds<BM, NU>::kUnits + 4 * w]);
+  if constexpr (!block_mode) {  // (written with the norm, before the barrier above, in decoder-block mode)
+    if (predict) {
+      for (int i = tid; i < BM * W; i += kOT) {  // tokens b..BM-1 are zero
+        const int t = i / W, w = i - t * W;
+        L.xw[i] = sign_word(&L.xs[t * OwnedLds<BM, NU>::kUnits + 4 * w]);
+      }
     }
+    __syncthreads();
   }
-  __syncthreads();
   SI_TRACE_MARK(1);
 
   // ---- 1. kept and confident masks of the owned rows, 64 rows per pass;
@@ -499,7 +502,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   // after the group exchange) is scaled and rounded now from the registers,
   // and the owner's tile of y starts as the residual h (while the finishing
   // wave publishes)
-  if (block_mode) {
+  if constexpr (block_mode) {
     if constexpr (kKeep) scale_x();
     if (owns_tile && wv == kTileWave) {
       const int half_cols = min(kTile, d - blk * kTile) / 2;
@@ -777,7 +780,7 @@ static int owned_rows_per_block(int k, int P, int tiles) {
   return (R + 7) / 8 * 8;
 }
 
-template <int BM, int NU>
+template <int BM, int NU, bool BLOCK = false>
 static int owned_blocks() {
   static int blocks = -1;
   if (blocks < 0) {
@@ -785,7 +788,7 @@ static int owned_blocks() {
     constexpr int lds = owned_lds_bytes<BM, NU>();
     if constexpr (lds <= kMaxLds) {
       int dev = 0, cus = 0, per_cu = 0;
-      const void* fn = reinterpret_cast<const void*>(&k_owned<BM, NU>);
+      const void* fn = reinterpret_cast<const void*>(&k_owned<BM, NU, BLOCK>);
       if (hipGetDevice(&dev) != hipSuccess) return 0;
       if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
       if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return 0;
@@ -804,7 +807,8 @@ static hipError_t owned_b(const LayerCall& c, hipStream_t s) {
     const int k = c.k, d = c.d;
     const WsLayout L = ws_layout(k, c.b);
     char* base = static_cast<char*>(c.ws);
-    const int P = owned_blocks<BM, NU>();
+    const bool block = c.h != nullptr;
+    const int P = block ? owned_blocks<BM, NU, true>() : owned_blocks<BM, NU, false>();
     if (P < 1) return hipErrorInvalidConfiguration;
     OwnedArgs a;
     a.signs = reinterpret_cast<const u32x4*>(c.signs);
@@ -836,7 +840,10 @@ static hipError_t owned_b(const LayerCall& c, hipStream_t s) {
     a.h = c.h;
     a.norm_w = c.norm_w;
     a.eps = c.eps;
-    k_owned<BM, NU><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
+    if (block)
+      k_owned<BM, NU, true><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
+    else
+      k_owned<BM, NU, false><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !c.counters || !c.y) return e;
     return launch_sum_counts(a.counts, P, c.n_out, k, c.counters, s);
