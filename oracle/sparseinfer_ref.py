@@ -22,6 +22,10 @@ check by eye against the paper:
 * Section III also names MLP blocks without step 2 (OPT, Falcon after
   ReLUfication): ``relu_mlp`` is that non-gated form,
   ``MLP(X) = ReLU(X W_fc1) W_down^T``, with the predictor on ``W_fc1``.
+* Section IV-A (robustness to quantization): the predictor needs only the
+  sign bit, so it applies to INT8 weights as they are; ``int8_mlp`` is
+  Eq. (1) with each weight taken as ``scale * q`` (symmetric per-row INT8,
+  ``quantize_rows_int8``) and ``pack_signs_int8`` packs the MSBs of ``q``.
 * Section IV-B 3)/4): the sparse GEMVs skip predicted-sparse rows of
   ``W_gate``, ``W_up`` and ``W_down^T``; "actual sparsity" additionally skips
   rows whose gate output is exactly zero.  Skipping a row whose value is zero
@@ -61,6 +65,11 @@ __all__ = [
     "relu_mlp",
     "rmsnorm_fp16",
     "mlp_block",
+    "quantize_rows_int8",
+    "sign_bits_int8",
+    "pack_signs_int8",
+    "dequantize_int8",
+    "int8_mlp",
     "dense_mlp",
     "gate_truly_positive",
     "prediction_quality",
@@ -294,6 +303,100 @@ def mlp_block(h, w_norm, eps: float, packed_w, w_gate, w_up, w_down, alpha: floa
     out["x"] = x
     out["mask"] = mask
     return out
+
+
+# ---------------------------------------------------------------------------
+# INT8 weights (Section IV-A: the predictor needs only the sign bit, so it
+# applies unchanged to INT8 weights)
+# ---------------------------------------------------------------------------
+
+def quantize_rows_int8(w):
+    """Symmetric per-row INT8 quantization of fp16 weights ``[rows][d]``
+    (bit patterns): ``scale_i = max_j |w_ij| / 127`` and
+    ``q_ij = rint(w_ij / scale_i)`` (ties to even), both in float32
+    arithmetic, ``q`` clamped to ``[-127, 127]``; a row of zeros has scale 0
+    and ``q = 0``.  Returns ``(q int8 [rows][d], scale float32 [rows])``.
+
+    The paper names INT8 without a scheme; one scale per row of the stored
+    matrix is a scale per output channel for ``W_gate`` and ``W_up``
+    (``[k][d]``) and for ``W_down`` (``[d][k]``)."""
+    W = fp16_to_f64(_as_u16(w)).astype(np.float32)
+    amax = np.max(np.abs(W), axis=1)
+    scale = (amax / np.float32(127.0)).astype(np.float32)
+    safe = np.where(scale > 0, scale, np.float32(1.0)).astype(np.float32)
+    q = np.rint((W / safe[:, None]).astype(np.float32))
+    q = np.clip(q, -127, 127).astype(np.int8)
+    q[scale == 0] = 0
+    return q, scale
+
+
+def sign_bits_int8(q) -> np.ndarray:
+    """The MSB of each INT8 weight (two's complement): 1 for negative values,
+    0 for zero and positive ones."""
+    return (np.asarray(q, dtype=np.int8).view(np.uint8) >> 7).astype(np.uint32)
+
+
+def pack_signs_int8(q) -> np.ndarray:
+    """Packed sign words of INT8 weights ``[rows][d]``, in the layout of
+    :func:`pack_signs`: bit ``j`` of word ``w`` is the MSB of element
+    ``32*w + j``; pad bits are 0."""
+    bits = sign_bits_int8(q)
+    rows, d = bits.shape
+    nw = (d + 31) // 32
+    padded = np.zeros((rows, nw * 32), dtype=np.uint64)
+    padded[:, :d] = bits
+    place = np.left_shift(np.uint64(1), np.arange(32, dtype=np.uint64))
+    return (padded.reshape(rows, nw, 32) * place).sum(axis=2).astype(np.uint32)
+
+
+def dequantize_int8(q, scale) -> np.ndarray:
+    """``scale_i * q_ij`` in float64 (exact: a float32 times an integer of
+    at most 8 bits)."""
+    return np.asarray(scale, dtype=np.float64)[:, None] * np.asarray(q, dtype=np.float64)
+
+
+def int8_mlp(q_gate, s_gate, q_up, s_up, q_down, s_down, x, mask):
+    """Eq. (1) over the kept rows with INT8 weights, every weight taken as
+    its dequantized value ``scale * q``.
+
+    ``q_gate``, ``q_up``: ``[k][d]`` int8 with per-row scales ``[k]``;
+    ``q_down``: ``[d][k]`` int8 (the paper's ``W_down``) with per-row scales
+    ``[d]``; ``q_up = None`` gives the non-gated ReLU MLP.  ``x``: ``[b][d]``
+    fp16 bits.  Returns ``y``, ``g``, ``h3`` and the work counters of
+    :func:`sparse_mlp` (``n_up = 0`` without ``W_up``)."""
+    q_gate = np.asarray(q_gate, dtype=np.int8)
+    q_down = np.asarray(q_down, dtype=np.int8)
+    xs = np.atleast_2d(_as_u16(x))
+    k, d = q_gate.shape
+    if q_down.shape != (d, k) or xs.shape[-1] != d:
+        raise ValueError("shape mismatch")
+    if q_up is not None and np.asarray(q_up).shape != (k, d):
+        raise ValueError("shape mismatch")
+    keep = active_rows(mask)
+    b = xs.shape[0]
+    X = fp16_to_f64(xs)                                    # [b][d]
+    Wg = dequantize_int8(q_gate, s_gate)[keep]             # [n][d]
+    WdT = dequantize_int8(q_down, s_down)[:, keep].T       # [n][d]: rows of W_down^T
+    g_kept = X @ Wg.T                                      # step 1, before sigma
+    h1_kept = np.maximum(g_kept, 0.0)                      # sigma = ReLU
+    if q_up is None:
+        h3_kept = h1_kept
+        n_up = 0
+    else:
+        u_kept = X @ dequantize_int8(q_up, s_up)[keep].T   # step 2
+        h3_kept = h1_kept * u_kept                         # step 3
+        n_up = int((h1_kept > 0).any(axis=0).sum())
+    y = h3_kept @ WdT                                      # step 4
+    g = np.zeros((b, k)); h3 = np.zeros((b, k))
+    g[:, keep] = g_kept; h3[:, keep] = h3_kept
+    return {
+        "y": y,
+        "g": g,
+        "h3": h3,
+        "n_gate": int(keep.size),
+        "n_up": n_up,
+        "n_down": int((h3_kept != 0).any(axis=0).sum()),
+    }
 
 
 def dense_mlp(w_gate, w_up, w_down, x):

@@ -530,3 +530,122 @@ def test_mlp_block_adds_the_residual():
     assert np.array_equal(oracle.mlp_block(h, wn, 1e-5, packed, wg, wu, zero_down, 1.0)["y"], h.astype(np.float64))
     relu = oracle.mlp_block(h, wn, 1e-5, packed, wg, None, wd, 1.0)
     assert np.array_equal(relu["mlp_y"], oracle.relu_mlp(wg, wd, x, mask)["y"])
+
+
+# ---------------------------------------------------------------------------
+# INT8 weights (Section IV-A: only the sign bit is needed, so the predictor
+# applies to INT8 weights unchanged)
+# ---------------------------------------------------------------------------
+
+def _int8_golden():
+    rows = []
+    rec = {}
+    cases = []
+    for l in _golden_lines("int8_worked_example.txt"):
+        if l[0] == "qrow":
+            arrow, colon = l.index("->"), l.index(":")
+            rows.append((list(map(float, l[2:arrow])), float(l[arrow + 1]), list(map(int, l[colon + 1:]))))
+        elif l[0] in ("gated", "relu"):
+            arrow = l.index("->")
+            cases.append((l[0], list(map(int, l[1:arrow])), list(map(float, l[arrow + 1:]))))
+        else:
+            rec[l[0]] = l[1:]
+    return rows, rec, cases
+
+
+def test_int8_quantization_golden_example():
+    rows, _, _ = _int8_golden()
+    w = np.stack([_bits(r) for r, _, _ in rows])
+    q, s = oracle.quantize_rows_int8(w)
+    assert q.dtype == np.int8 and s.dtype == np.float32
+    for i, (_, scale, want) in enumerate(rows):
+        assert float(s[i]) == scale
+        assert q[i].tolist() == want
+    # the MSB of an INT8 zero is 0, whatever the sign of the weight it came from
+    assert oracle.sign_bits_int8(q)[0].tolist() == [0, 1, 0, 0, 0, 0]
+
+
+def test_int8_mlp_golden_example():
+    _, rec, cases = _int8_golden()
+    def mat(tokens):
+        return np.array([list(map(int, part.split())) for part in " ".join(tokens).split("|")], dtype=np.int8)
+    x = _bits(map(float, rec["x"]))[None, :]
+    qg, qu, qd = mat(rec["gate"]), mat(rec["up"]), mat(rec["down"])
+    sg, su, sd = (np.array(list(map(float, rec[n])), dtype=np.float32) for n in ("sgate", "sup", "sdown"))
+    for kind, mask, (y0, y1, ng, nu, nd) in cases:
+        m = np.array(mask, dtype=np.uint8)
+        out = oracle.int8_mlp(qg, sg, qu if kind == "gated" else None, su, qd, sd, x, m)
+        assert out["y"][0].tolist() == [y0, y1]
+        assert (out["n_gate"], out["n_up"], out["n_down"]) == (ng, nu, nd)
+
+
+@pytest.mark.parametrize("d", [1, 5, 31, 32, 33, 64, 100])
+def test_int8_sign_packing_bit_by_bit_and_as_fp16(d):
+    rng = np.random.default_rng(300 + d)
+    q = rng.integers(-128, 128, size=(6, d)).astype(np.int8)
+    q[:, ::3] = 0
+    packed = oracle.pack_signs_int8(q)
+    for i in range(6):
+        for j in range(d):
+            assert (int(packed[i, j // 32]) >> (j % 32)) & 1 == (1 if int(q[i, j]) < 0 else 0)
+        for j in range(d, 32 * packed.shape[1]):
+            assert (int(packed[i, j // 32]) >> (j % 32)) & 1 == 0
+    # every INT8 value is an fp16 value with the same sign bit (0 -> +0)
+    assert np.array_equal(packed, oracle.pack_signs(q.astype(np.float16)))
+
+
+def test_int8_quantization_invariants():
+    rng = np.random.default_rng(31)
+    w = _random_bits(rng, (40, 96), special=True)
+    w[3] = 0
+    w[4] = 0x8000  # a row of -0
+    q, s = oracle.quantize_rows_int8(w)
+    W = oracle.fp16_to_f64(w)
+    assert np.all(np.abs(q.astype(int)) <= 127)
+    nz = np.max(np.abs(W), axis=1) > 0
+    assert np.array_equal(nz, s > 0)
+    assert np.all(np.max(np.abs(q[nz].astype(int)), axis=1) == 127)
+    assert np.all(q[~nz] == 0)
+    # rounding to nearest: |w - s q| <= s / 2, up to the float32 quotient's rounding
+    err = np.abs(W - oracle.dequantize_int8(q, s))
+    assert np.all(err <= s.astype(np.float64)[:, None] * (0.5 + 64 * 2.0 ** -24))
+    # the sign survives wherever q is not 0
+    qs = q.astype(int)
+    assert np.all((qs[qs != 0] < 0) == (W[qs != 0] < 0))
+
+
+def test_int8_quantization_is_lossless_on_scaled_integers():
+    """A row of fp16 values q0 * 2^e with max |q0| = 127 has scale 2^e exactly
+    and quantizes back to q0."""
+    rng = np.random.default_rng(32)
+    q0 = rng.integers(-127, 128, size=(12, 50)).astype(np.int8)
+    q0[:, 7] = np.where(rng.random(12) < 0.5, 127, -127)
+    e = rng.integers(-12, 3, size=12)
+    w = (q0.astype(np.float64) * (2.0 ** e)[:, None]).astype(np.float16)
+    assert np.array_equal(w.astype(np.float64), q0.astype(np.float64) * (2.0 ** e)[:, None])
+    q, s = oracle.quantize_rows_int8(w)
+    assert np.array_equal(q, q0) and np.array_equal(s, (2.0 ** e).astype(np.float32))
+
+
+@pytest.mark.parametrize("k,d,b", [(24, 24, 1), (40, 16, 3), (17, 64, 2)])
+def test_int8_mlp_is_the_fp16_mlp_of_its_dequantized_weights(k, d, b):
+    """With power-of-two scales every dequantized weight is an fp16 value, so
+    the INT8 MLP must equal the fp16 MLP of those values exactly (per-row
+    scales that differ from row to row, and d == k, expose a scale taken along
+    the wrong axis)."""
+    rng = np.random.default_rng(k * 7 + d)
+    qg, qu = (rng.integers(-127, 128, size=(k, d)).astype(np.int8) for _ in range(2))
+    qd = rng.integers(-127, 128, size=(d, k)).astype(np.int8)
+    sg, su = ((2.0 ** rng.integers(-9, 1, size=k)).astype(np.float32) for _ in range(2))
+    sd = (2.0 ** rng.integers(-9, 1, size=d)).astype(np.float32)
+    fp = [(oracle.dequantize_int8(q, s)).astype(np.float16) for q, s in ((qg, sg), (qu, su), (qd, sd))]
+    x = _random_bits(rng, (b, d), special=False)
+    for mask in [np.ones(k, np.uint8), (rng.random(k) < 0.4).astype(np.uint8), np.zeros(k, np.uint8)]:
+        a = oracle.int8_mlp(qg, sg, qu, su, qd, sd, x, mask)
+        r = oracle.sparse_mlp(fp[0], fp[1], fp[2], x, mask)
+        assert np.array_equal(a["y"], r["y"]) and np.array_equal(a["h3"], r["h3"])
+        assert (a["n_gate"], a["n_up"], a["n_down"]) == (r["n_gate"], r["n_up"], r["n_down"])
+        a = oracle.int8_mlp(qg, sg, None, None, qd, sd, x, mask)
+        r = oracle.relu_mlp(fp[0], fp[2], x, mask)
+        assert np.array_equal(a["y"], r["y"]) and np.array_equal(a["h3"], r["h"])
+        assert (a["n_gate"], a["n_up"], a["n_down"]) == (r["n_gate"], 0, r["n_down"])
