@@ -8,7 +8,9 @@ actual sparsity and sparse down-projection, for the 7B-shaped layer
 layer (d = 4096, k = 16384) instead, same sparsity and alpha; ``--mlp block``
 times the 7B layer as a decoder-block call (RMSNorm of the fp32 residual
 stream and the residual add fused around the path) and, for comparison, the
-plain call on the same layers.
+plain call on the same layers; ``--mlp int8`` times the 7B layer with INT8
+weights (symmetric, one scale per output channel, quantized on the device at
+load; the predictor reads the MSBs of the INT8 W_gate).
 Steps cycle through a pool of independently seeded layers whose weights
 (>= 4.4 GB) exceed the 256 MB Infinity Cache, so every step reads its bytes
 from HBM.  The timed loop is replayed from a HIP graph (the per-call host
@@ -39,20 +41,25 @@ HBM_PEAK_GBS = 8000.0
 # the non-gated workload (--mlp relu): OPT-6.7B's MLP shape
 RELU_METRIC = "µs per non-gated ReLU MLP layer (predict+sparse GEMV) at OPT-6.7B shape, s=0.9; effective HBM GB/s"
 RELU_D, RELU_K = 4096, 16384
+INT8_METRIC = "µs per MLP layer with INT8 weights (predict+sparse GEMV) at 7B shape, s=0.9; effective HBM GB/s"
 BLOCK_METRIC = ("µs per decoder-block MLP call (RMSNorm + predict + sparse GEMV + residual) at 7B shape, s=0.9; "
                 "effective HBM GB/s")
 
 
-def algorithmic_bytes(k, d, b, n_gate, n_up, n_down, block=False):
+def algorithmic_bytes(k, d, b, n_gate, n_up, n_down, block=False, int8=False):
     """Bytes the method itself must move for one layer and one step (the
     decoder-block call reads the fp32 residual stream and the norm weight
-    instead of the fp16 x)."""
+    instead of the fp16 x; INT8 rows are d bytes, plus the float scales of
+    the kept W_gate / W_up rows and the d scales of the columns of y)."""
     x_bytes = 4 * d * b + 4 * d if block else 2 * d * b
+    if int8:
+        return k * d // 8 + x_bytes + d * (n_gate + n_up + n_down) + 4 * (n_gate + n_up) + 4 * d + 4 * d * b
     return k * d // 8 + x_bytes + 2 * d * (n_gate + n_up + n_down) + 4 * d * b
 
 
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_7b_s0.9_counters.txt")
 RELU_COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_opt6.7b_relu_s0.9_counters.txt")
+INT8_COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_7b_int8_s0.9_counters.txt")
 KERNEL_SOURCES = ("paper_2411_12692_amd/csrc/owned.hip", "paper_2411_12692_amd/csrc/layer_common.h",
                   "paper_2411_12692_amd/csrc/si_device.h")
 
@@ -91,9 +98,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=256)
     ap.add_argument("--layers", type=int, default=16, help="size of the rotating layer pool")
     ap.add_argument("--alpha", type=float, default=1.0)
-    ap.add_argument("--mlp", choices=("gated", "relu", "block"), default="gated",
+    ap.add_argument("--mlp", choices=("gated", "relu", "block", "int8"), default="gated",
                     help="gated: the 7B-shaped gated MLP (default); relu: the non-gated ReLU MLP of an "
-                         "OPT-6.7B-shaped layer; block: the 7B layer with RMSNorm and residual fused")
+                         "OPT-6.7B-shaped layer; block: the 7B layer with RMSNorm and residual fused; int8: the "
+                         "7B layer with INT8 weights")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--launches", type=int, default=256, help="individually timed launches for the roofline")
@@ -120,12 +128,14 @@ def profile_pass(step, n_layers, calls, dev):
     print(f"# profile pass: {calls} layer calls, 4 copies of {src.numel() * 2} bytes", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None):
+def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None, int8=False):
     """Time the CPU oracle (test infrastructure, never tuned) on a bounded
     sample of the same workload: predict + masked MLP on the first layers of
     the pool, repeated until the budget is spent, with one BLAS thread
     (``wu is None``: the non-gated MLP; ``block`` = per-layer ``(h, norm_w,
-    eps)``: the decoder-block form, RMSNorm and residual included)."""
+    eps)``: the decoder-block form, RMSNorm and residual included; ``int8``:
+    the entries hold the oracle's INT8 weights and scales, quantized beforehand,
+    untimed, as at load)."""
     from threadpoolctl import threadpool_limits
 
     import oracle
@@ -135,7 +145,11 @@ def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None):
         while total_s < budget_s:
             for li, (wg, wu, wd, x, packed) in enumerate(layers_host):
                 t0 = time.perf_counter()
-                if block is not None:
+                if int8:
+                    mask, _, _ = oracle.predict_rows(packed, x, alpha)
+                    (qg, sg), (qu, su), (qd, sd) = wg, wu, wd
+                    out = oracle.int8_mlp(qg, sg, qu, su, qd, sd, x, mask)
+                elif block is not None:
                     h, nw, eps = block[li]
                     out = oracle.mlp_block(h, nw, eps, packed, wg, wu, wd, alpha)
                 else:
@@ -147,10 +161,11 @@ def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None):
                 total_s += time.perf_counter() - t0
                 calls += 1
                 total_bytes += algorithmic_bytes(k, d, x.shape[0], out["n_gate"], out["n_up"], out["n_down"],
-                                                 block=block is not None)
+                                                 block=block is not None, int8=int8)
                 if total_s >= budget_s:
                     break
     what = ("rmsnorm_fp16 + predict_rows + sparse_mlp + residual" if block is not None else
+            "predict_rows on pack_signs_int8 + int8_mlp" if int8 else
             f"predict_rows + {'relu_mlp' if layers_host[0][1] is None else 'sparse_mlp'}")
     return {
         "value": round(total_bytes / total_s / 1e9, 3),
@@ -224,6 +239,7 @@ def main():
 
     relu = args.mlp == "relu"
     block = args.mlp == "block"
+    int8 = args.mlp == "int8"
     D_, K_ = (RELU_D, RELU_K) if relu else (D, K)
     EPS = 1e-5
     L = args.layers
@@ -231,7 +247,10 @@ def main():
     for l in range(L):
         # the non-gated layer takes the planted W_gate as its W_fc1
         pl = synth.planted_layer(D_, K_, S, config=7 if relu else 2, layer=l, device=dev)
-        layers.append(si.MLPLayer(pl.w_gate, None if relu else pl.w_up, pl.w_down))
+        if int8:  # quantized on the device, as at load
+            layers.append(si.Int8MLPLayer(pl.w_gate, pl.w_up, pl.w_down))
+        else:
+            layers.append(si.MLPLayer(pl.w_gate, None if relu else pl.w_up, pl.w_down))
         xs.append(pl.x)
         if block:
             # residual stream with the planted token's signs, positive norm weight
@@ -244,7 +263,12 @@ def main():
             wg, wd, xh = u16(pl.w_gate), u16(pl.w_down), u16(pl.x)
             wu = None if relu else u16(pl.w_up)
             import oracle
-            host.append((wg, wu, wd, xh, oracle.pack_signs(wg)))
+            if int8:
+                qg = oracle.quantize_rows_int8(wg)
+                host.append((qg, oracle.quantize_rows_int8(wu), oracle.quantize_rows_int8(wd), xh,
+                             oracle.pack_signs_int8(qg[0])))
+            else:
+                host.append((wg, wu, wd, xh, oracle.pack_signs(wg)))
             if block:
                 host_block.append((hs[-1].cpu().numpy(), nws[-1].cpu().numpy(), EPS))
         del pl
@@ -269,7 +293,7 @@ def main():
     if args.profile_pass:
         profile_pass(step, L, max(args.launches, L), dev)
         return
-    bytes_per_layer = [algorithmic_bytes(K_, D_, 1, *c, block=block) for c in counts]
+    bytes_per_layer = [algorithmic_bytes(K_, D_, 1, *c, block=block, int8=int8) for c in counts]
     mean_bytes = sum(bytes_per_layer) / L
 
     us_per_layer, steps, warmup, wall_us = time_graph(step, L, args.steps, args.warmup)
@@ -300,7 +324,7 @@ def main():
     isolated_us = sum(a.elapsed_time(b) * 1e3 for a, b in evs) / M
 
     result = {
-        "metric": RELU_METRIC if relu else BLOCK_METRIC if block else METRIC,
+        "metric": RELU_METRIC if relu else BLOCK_METRIC if block else INT8_METRIC if int8 else METRIC,
         "value": round(mean_bytes / us_per_layer / 1e3, 2),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -311,13 +335,15 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16",
+        "dtype": "i8" if int8 else "f16",
         "accumulate": "f32",
         "data": "synthetic",
         "config": {
             "workload": (f"OPT-6.7B-shaped non-gated ReLU MLP layer (no W_up) d={D_} k={K_}" if relu else
                          f"7B-shaped ReLU gated MLP layer d={D_} k={K_} as a decoder-block call (RMSNorm of the "
                          f"fp32 residual stream, eps={EPS}, and the residual add fused)" if block else
+                         f"7B-shaped ReLU gated MLP layer d={D_} k={K_} with INT8 weights (symmetric, one float "
+                         f"scale per output channel, quantized on the device; fp16 x, fp32 accumulation)" if int8 else
                          f"7B-shaped ReLU gated MLP layer d={D_} k={K_}") +
                         f", planted sparsity s={S}, alpha={args.alpha}, batch 1, rotating pool of {L} layers, "
                         f"HIP-graph replay",
@@ -332,7 +358,8 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None if block else measured_traffic(RELU_COUNTERS_FILE if relu else COUNTERS_FILE),
+            "traffic": None if block else measured_traffic(RELU_COUNTERS_FILE if relu else
+                                                           INT8_COUNTERS_FILE if int8 else COUNTERS_FILE),
             "launch_us": round(us_per_layer, 3),
             "isolated_launch_us": round(isolated_us, 3),
         },
@@ -341,7 +368,7 @@ def main():
         result["plain_call_us"] = round(plain_us, 3)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(host, args.alpha, args.cpu_seconds, K_, D_,
-                                              block=host_block if block else None)
+                                              block=host_block if block else None, int8=int8)
     print(json.dumps(result), flush=True)
 
 

@@ -225,6 +225,80 @@ si_status si_rmsnorm_predict_sparse_mlp(const float* h, const float* norm_w, flo
                                         int32_t* n_active, float* y, void* workspace, size_t workspace_bytes,
                                         uint32_t flags, int32_t* counters, void* stream);
 
+/*
+ * INT8 weights.  The predictor reads only the sign bit of each weight, so it
+ * applies to INT8 weights unchanged (Section IV-A, robustness to the
+ * quantization scheme): the MSB of a two's-complement INT8 value is its
+ * sign (0 for zero).  The paper names INT8 without a scheme; these entry
+ * points use symmetric INT8 with one float32 scale per output channel, each
+ * weight standing for scale * q:
+ *   W_gate, W_up : [k][d] int8, scales [k] (one per row);
+ *   W_down       : [d][k] int8 (the paper's layout), scales [d] (one per row,
+ *                  i.e. per column of y); the kernels take its transpose
+ *                  W_down^T [k][d] int8 (si_transpose_down_i8) and the
+ *                  same [d] scales.
+ */
+
+/*
+ * Symmetric per-row quantization, once at load: for each of `rows` rows of
+ * n fp16 values, scale = max_j |w_j| / 127 and q_j = rint(w_j / scale)
+ * (ties to even, clamped to [-127, 127]), computed in float32 with
+ * correctly rounded division; a row of zeros gets scale 0 and q = 0.
+ *   w     : [rows][n] fp16, read.       q : [rows][n] int8, written.
+ *   scale : [rows] float32, written.    1 <= rows, n <= 2^24 (n need not be
+ *   a multiple of anything; only the base pointers must be aligned).
+ */
+si_status si_quantize_rows_i8(const uint16_t* w, int rows, int n, int8_t* q, float* scale, void* stream);
+
+/*
+ * Pack the sign bits (MSBs) of INT8 W_gate (or W_fc1), once at load.
+ * w_gate : [k][d] int8, read.  signs : si_signs_bytes(k, d) bytes, written,
+ * in the same private layout as si_pack_signs (si_signs_to_canonical
+ * exports it); si_predict accepts them as they are.
+ */
+si_status si_pack_signs_i8(const int8_t* w_gate, int k, int d, uint32_t* signs, void* stream);
+
+/*
+ * INT8 W_down [d][k] -> W_down^T [k][d], once at load (the buffers must not
+ * overlap).
+ */
+si_status si_transpose_down_i8(const int8_t* w_down, int d, int k, int8_t* w_down_t, void* stream);
+
+/*
+ * Eq. (1) over the rows kept by a caller's mask with INT8 weights (the INT8
+ * form of si_sparse_mlp / si_sparse_relu_mlp in mask mode).  For every kept
+ * row i and token t:
+ *   g = s_gate[i] * (q_gate,i . x_t) ; h1 = max(g, 0) ;
+ *   u = s_up[i] * (q_up,i . x_t)  (read only when some token has h1 > 0) ;
+ *   h3 = h1 * u ;  y_t[j] += s_down[j] * sum_i h3_i * q_downT[i][j]
+ *   (rows read only when some token has h3 != 0).
+ * w_up == NULL (s_up ignored) runs the non-gated ReLU MLP (h3 = h1).
+ *   mask    : [k] uint8, nonzero = kept (required).
+ *   y       : [b][d] float32, overwritten.
+ * Flags, counters, workspace and errors as si_sparse_mlp.  Runs where the
+ * single-launch path applies (si_single_launch(k, d, b) == 1); other shapes
+ * return SI_ERR_SHAPE.
+ */
+si_status si_sparse_mlp_i8(const int8_t* w_gate, const float* s_gate, const int8_t* w_up, const float* s_up,
+                           const int8_t* w_down_t, const float* s_down, int k, int d, const uint16_t* x, int b,
+                           const uint8_t* mask, float* y, void* workspace, size_t workspace_bytes, uint32_t flags,
+                           int32_t* counters, void* stream);
+
+/*
+ * The whole per-token path with INT8 weights: si_predict on the signs of
+ * the INT8 W_gate (si_pack_signs_i8) followed by si_sparse_mlp_i8 over the
+ * predicted rows, in one launch, with the arguments and outputs of
+ * si_predict_sparse_mlp (mask, active_idx, n_active and counters may each be
+ * NULL; w_up == NULL: the non-gated ReLU MLP).  Runs where the
+ * single-launch path applies; other shapes return SI_ERR_SHAPE.
+ */
+si_status si_predict_sparse_mlp_i8(const uint32_t* signs, const int8_t* w_gate, const float* s_gate,
+                                   const int8_t* w_up, const float* s_up, const int8_t* w_down_t,
+                                   const float* s_down, int k, int d, const uint16_t* x, int b, float alpha,
+                                   uint8_t* mask, int32_t* active_idx, int32_t* n_active, float* y,
+                                   void* workspace, size_t workspace_bytes, uint32_t flags, int32_t* counters,
+                                   void* stream);
+
 #ifdef __cplusplus
 }
 #endif

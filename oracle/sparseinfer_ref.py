@@ -375,15 +375,17 @@ def int8_mlp(q_gate, s_gate, q_up, s_up, q_down, s_down, x, mask):
     keep = active_rows(mask)
     b = xs.shape[0]
     X = fp16_to_f64(xs)                                    # [b][d]
-    Wg = dequantize_int8(q_gate, s_gate)[keep]             # [n][d]
-    WdT = dequantize_int8(q_down, s_down)[:, keep].T       # [n][d]: rows of W_down^T
+    s_gate = np.asarray(s_gate)
+    Wg = dequantize_int8(q_gate[keep], s_gate[keep])       # [n][d]
+    WdT = dequantize_int8(q_down[:, keep], s_down).T       # [n][d]: rows of W_down^T
     g_kept = X @ Wg.T                                      # step 1, before sigma
     h1_kept = np.maximum(g_kept, 0.0)                      # sigma = ReLU
     if q_up is None:
         h3_kept = h1_kept
         n_up = 0
     else:
-        u_kept = X @ dequantize_int8(q_up, s_up)[keep].T   # step 2
+        q_up = np.asarray(q_up, dtype=np.int8)
+        u_kept = X @ dequantize_int8(q_up[keep], np.asarray(s_up)[keep]).T   # step 2
         h3_kept = h1_kept * u_kept                         # step 3
         n_up = int((h1_kept > 0).any(axis=0).sum())
     y = h3_kept @ WdT                                      # step 4

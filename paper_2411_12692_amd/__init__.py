@@ -20,6 +20,8 @@ __all__ = [
     "SI_NO_AS", "SI_NO_SPECULATION", "SparseInferError", "signs_bytes", "alpha_threshold", "workspace_bytes",
     "new_workspace", "pack_signs", "signs_to_canonical", "transpose_down", "predict",
     "sparse_mlp", "predict_sparse_mlp", "mlp_block", "MLPLayer",
+    "quantize_rows_i8", "pack_signs_i8", "transpose_down_i8", "sparse_mlp_i8", "predict_sparse_mlp_i8",
+    "Int8MLPLayer",
 ]
 
 
@@ -238,3 +240,122 @@ class MLPLayer:
     def sparse_mlp(self, x, mask=None, active_idx=None, n_active=None, flags: int = 0, counters: bool = False):
         return sparse_mlp(self.w_gate, self.w_up, self.w_down_t, x, self.workspace, mask, active_idx, n_active,
                           flags, counters)
+
+
+# ---- INT8 weights ---------------------------------------------------------
+
+def quantize_rows_i8(w: torch.Tensor):
+    """Symmetric per-row INT8 quantization of fp16 ``w [rows][n]``: returns
+    ``(q int8 [rows][n], scale float32 [rows])`` (``si_quantize_rows_i8``)."""
+    _dev(w, "w", _F16, 2)
+    rows, n = w.shape
+    q = torch.empty(rows, n, dtype=torch.int8, device=w.device)
+    scale = torch.empty(rows, dtype=torch.float32, device=w.device)
+    _lib.call("si_quantize_rows_i8", _vp(w), rows, n, _vp(q), _vp(scale), _stream())
+    return q, scale
+
+
+def pack_signs_i8(q_gate: torch.Tensor) -> torch.Tensor:
+    """Packed MSBs of INT8 ``W_gate [k][d]`` (the layout of ``pack_signs``)."""
+    _dev(q_gate, "q_gate", (torch.int8,), 2)
+    k, d = q_gate.shape
+    nbytes = signs_bytes(k, d)
+    if nbytes == 0:
+        raise ValueError(f"unsupported shape k={k} d={d}")
+    out = torch.empty(nbytes // 4, dtype=torch.int32, device=q_gate.device)
+    _lib.call("si_pack_signs_i8", _vp(q_gate), k, d, _vp(out), _stream())
+    return out
+
+
+def transpose_down_i8(q_down: torch.Tensor) -> torch.Tensor:
+    """INT8 ``W_down [d][k]`` -> ``W_down^T [k][d]``."""
+    _dev(q_down, "q_down", (torch.int8,), 2)
+    d, k = q_down.shape
+    out = torch.empty(k, d, dtype=torch.int8, device=q_down.device)
+    _lib.call("si_transpose_down_i8", _vp(q_down), d, k, _vp(out), _stream())
+    return out
+
+
+def _i8_weights(q_gate, s_gate, q_up, s_up, q_down_t, s_down):
+    _dev(q_gate, "q_gate", (torch.int8,), 2)
+    _dev(q_down_t, "q_down_t", (torch.int8,), 2)
+    k, d = q_gate.shape
+    _dev(s_gate, "s_gate", (torch.float32,), 1)
+    _dev(s_down, "s_down", (torch.float32,), 1)
+    if q_up is not None:
+        _dev(q_up, "q_up", (torch.int8,), 2)
+        _dev(s_up, "s_up", (torch.float32,), 1)
+        if tuple(q_up.shape) != (k, d) or s_up.numel() != k:
+            raise ValueError("q_up / s_up do not match q_gate")
+    if tuple(q_down_t.shape) != (k, d) or s_gate.numel() != k or s_down.numel() != d:
+        raise ValueError("q_down_t [k][d], s_gate [k] and s_down [d] expected")
+    return k, d
+
+
+def sparse_mlp_i8(q_gate, s_gate, q_up, s_up, q_down_t, s_down, x, workspace, mask, flags: int = 0,
+                  counters: bool = False):
+    """Eq. (1) over the rows kept by ``mask`` with INT8 weights
+    (``si_sparse_mlp_i8``); ``q_up=None``: the non-gated ReLU MLP.  Returns
+    ``y [b][d]`` float32 (and the ``[3]`` work counters with ``counters``)."""
+    k, d = _i8_weights(q_gate, s_gate, q_up, s_up, q_down_t, s_down)
+    x = _x2(x, d)
+    b = x.shape[0]
+    y = torch.empty(b, d, dtype=torch.float32, device=x.device)
+    cnt = torch.zeros(3, dtype=torch.int32, device=x.device) if counters else None
+    _lib.call("si_sparse_mlp_i8", _vp(q_gate), _vp(s_gate), _vp(q_up), _vp(s_up if q_up is not None else None),
+              _vp(q_down_t), _vp(s_down), k, d, _vp(x), b, _vp(mask), _vp(y), _vp(workspace), workspace.numel(),
+              flags, _vp(cnt), _stream())
+    return (y, cnt) if counters else y
+
+
+def predict_sparse_mlp_i8(signs, q_gate, s_gate, q_up, s_up, q_down_t, s_down, x, alpha, workspace,
+                          flags: int = 0, outputs: bool = False, y: torch.Tensor = None):
+    """The whole per-token path with INT8 weights
+    (``si_predict_sparse_mlp_i8``); ``signs`` from ``pack_signs_i8``.
+    Returns ``y`` (and ``(mask, active_idx, n_active, counters)`` with
+    ``outputs``)."""
+    k, d = _i8_weights(q_gate, s_gate, q_up, s_up, q_down_t, s_down)
+    _dev(signs, "signs", (torch.int32,))
+    x = _x2(x, d)
+    b = x.shape[0]
+    if y is None:
+        y = torch.empty(b, d, dtype=torch.float32, device=x.device)
+    else:
+        _dev(y, "y", (torch.float32,))
+        if y.numel() != b * d:
+            raise ValueError(f"y must hold [{b}][{d}] floats")
+    if outputs:
+        mask = torch.empty(k, dtype=torch.uint8, device=x.device)
+        idx = torch.empty(k, dtype=torch.int32, device=x.device)
+        n = torch.empty(1, dtype=torch.int32, device=x.device)
+        cnt = torch.zeros(3, dtype=torch.int32, device=x.device)
+    else:
+        mask = idx = n = cnt = None
+    _lib.call("si_predict_sparse_mlp_i8", _vp(signs), _vp(q_gate), _vp(s_gate), _vp(q_up),
+              _vp(s_up if q_up is not None else None), _vp(q_down_t), _vp(s_down), k, d, _vp(x), b, float(alpha),
+              _vp(mask), _vp(idx), _vp(n), _vp(y), _vp(workspace), workspace.numel(), flags, _vp(cnt), _stream())
+    return (y, (mask, idx, n, cnt)) if outputs else y
+
+
+class Int8MLPLayer:
+    """One layer with INT8 weights, made on the device at load from fp16
+    weights: per-row quantization of ``W_gate``, ``W_up`` (``[k][d]``) and
+    ``W_down`` (``[d][k]``), the packed MSBs of the INT8 ``W_gate`` and the
+    INT8 ``W_down^T``.  ``w_up=None``: a non-gated ReLU MLP."""
+
+    def __init__(self, w_gate: torch.Tensor, w_up: torch.Tensor, w_down: torch.Tensor, max_batch: int = 1):
+        self.k, self.d = w_gate.shape
+        self.q_gate, self.s_gate = quantize_rows_i8(w_gate)
+        self.q_up, self.s_up = quantize_rows_i8(w_up) if w_up is not None else (None, None)
+        q_down, self.s_down = quantize_rows_i8(w_down)
+        self.q_down_t = transpose_down_i8(q_down)
+        self.signs = pack_signs_i8(self.q_gate)
+        self.workspace = new_workspace(self.k, self.d, max_batch, w_gate.device)
+
+    def __call__(self, x, alpha: float, flags: int = 0, outputs: bool = False, y: torch.Tensor = None):
+        return predict_sparse_mlp_i8(self.signs, self.q_gate, self.s_gate, self.q_up, self.s_up, self.q_down_t,
+                                     self.s_down, x, alpha, self.workspace, flags=flags, outputs=outputs, y=y)
+
+    def sparse_mlp(self, x, mask, flags: int = 0, counters: bool = False):
+        return sparse_mlp_i8(self.q_gate, self.s_gate, self.q_up, self.s_up, self.q_down_t, self.s_down, x,
+                             self.workspace, mask, flags, counters)

@@ -48,6 +48,12 @@ SIGNATURES = {
     "si_sparse_relu_mlp": (_i, [_p, _p, _i, _i, _p, _i, _p, _p, _p, _p, _p, _sz, _u32, _p, _p]),
     "si_predict_sparse_relu_mlp": (_i, [_p, _p, _p, _i, _i, _p, _i, _f, _p, _p, _p, _p, _p, _sz, _u32,
                                         _p, _p]),
+    "si_quantize_rows_i8": (_i, [_p, _i, _i, _p, _p, _p]),
+    "si_pack_signs_i8": (_i, [_p, _i, _i, _p, _p]),
+    "si_transpose_down_i8": (_i, [_p, _i, _i, _p, _p]),
+    "si_sparse_mlp_i8": (_i, [_p, _p, _p, _p, _p, _p, _i, _i, _p, _i, _p, _p, _p, _sz, _u32, _p, _p]),
+    "si_predict_sparse_mlp_i8": (_i, [_p, _p, _p, _p, _p, _p, _p, _i, _i, _p, _i, _f, _p, _p, _p, _p, _p, _sz,
+                                      _u32, _p, _p]),
     "si_rmsnorm_predict_sparse_mlp": (_i, [_p, _p, _f, _p, _p, _p, _p, _i, _i, _i, _f, _p, _p, _p, _p, _p, _sz,
                                            _u32, _p, _p]),
 }

@@ -388,3 +388,133 @@ si_status si_rmsnorm_predict_sparse_mlp(const float* h, const float* norm_w, flo
 }
 
 }  // extern "C"
+
+// ---- INT8 weights ---------------------------------------------------------
+
+namespace {
+
+// si_sparse_mlp_i8 (mask given, predict == false) and si_predict_sparse_mlp_i8.
+si_status int8_impl(bool predict, const uint32_t* signs, const int8_t* w_gate, const float* s_gate,
+                    const int8_t* w_up, const float* s_up, const int8_t* w_down_t, const float* s_down, int k,
+                    int d, const uint16_t* x, int b, float alpha, const uint8_t* mask_in, uint8_t* mask,
+                    int32_t* active_idx, int32_t* n_active, float* y, void* workspace, size_t workspace_bytes,
+                    uint32_t flags, int32_t* counters, void* stream) {
+  if (predict) {
+    REQUIRE_PTR(signs);
+  } else {
+    REQUIRE_PTR(mask_in);
+  }
+  REQUIRE_PTR(w_gate);
+  REQUIRE_PTR(s_gate);
+  REQUIRE_PTR(w_down_t);
+  REQUIRE_PTR(s_down);
+  REQUIRE_PTR(x);
+  REQUIRE_PTR(y);
+  if (w_up) REQUIRE_PTR(s_up);
+  REQUIRE_ALIGNED(signs);
+  REQUIRE_ALIGNED(w_gate);
+  REQUIRE_ALIGNED(s_gate);
+  REQUIRE_ALIGNED(w_up);
+  REQUIRE_ALIGNED(s_up);
+  REQUIRE_ALIGNED(w_down_t);
+  REQUIRE_ALIGNED(s_down);
+  REQUIRE_ALIGNED(x);
+  REQUIRE_ALIGNED(y);
+  REQUIRE_ALIGNED(mask_in);
+  REQUIRE_ALIGNED(mask);
+  REQUIRE_ALIGNED(active_idx);
+  REQUIRE_ALIGNED(n_active);
+  REQUIRE_ALIGNED(counters);
+  if (flags & ~(SI_NO_AS | SI_NO_SPECULATION)) return fail(SI_ERR_FLAGS, "unknown flags 0x%x", flags);
+  if (si_status s = check_kd(k, d)) return s;
+  if (si_status s = check_b(b)) return s;
+  if (predict && (std::isnan(alpha) || alpha < 0.0f))
+    return fail(SI_ERR_ALPHA, "alpha=%g must be >= 0 (or +inf)", (double)alpha);
+  if (si_status s = check_ws(workspace, workspace_bytes, k, b)) return s;
+  if (!si::owned_supported(k, d, b))
+    return fail(SI_ERR_SHAPE, "k=%d d=%d b=%d: INT8 weights need the single-launch path", k, d, b);
+  char* base = static_cast<char*>(workspace);
+  si::LayerCall c;
+  c.signs = predict ? signs : nullptr;
+  c.mask_in = predict ? nullptr : mask_in;
+  c.w_gate = reinterpret_cast<const uint16_t*>(w_gate);
+  c.w_up = reinterpret_cast<const uint16_t*>(w_up);
+  c.w_down_t = reinterpret_cast<const uint16_t*>(w_down_t);
+  c.i8 = true;
+  c.s_gate = s_gate;
+  c.s_up = w_up ? s_up : nullptr;
+  c.s_down = s_down;
+  c.x = x;
+  c.k = k;
+  c.d = d;
+  c.b = b;
+  if (predict) {
+    c.T = si_alpha_threshold(alpha, d);
+    c.margin = d / 16;
+    c.mask = mask;
+    c.idx = active_idx;
+  }
+  c.n_out = predict && n_active ? n_active : reinterpret_cast<int32_t*>(base) + si::H_N_INTERNAL;
+  c.flags = flags;
+  c.y = y;
+  c.ws = workspace;
+  c.counters = counters;
+  return hip_status(si::launch_owned(c, (hipStream_t)stream), "INT8 layer launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+si_status si_quantize_rows_i8(const uint16_t* w, int rows, int n, int8_t* q, float* scale, void* stream) {
+  REQUIRE_PTR(w);
+  REQUIRE_PTR(q);
+  REQUIRE_PTR(scale);
+  REQUIRE_ALIGNED(w);
+  REQUIRE_ALIGNED(q);
+  REQUIRE_ALIGNED(scale);
+  if (rows < 1 || rows > (1 << 24) || n < 1 || n > (1 << 24))
+    return fail(SI_ERR_SHAPE, "rows=%d n=%d outside [1, 2^24]", rows, n);
+  return hip_status(si::launch_quantize_rows(w, rows, n, q, scale, (hipStream_t)stream), "quantize launch");
+}
+
+si_status si_pack_signs_i8(const int8_t* w_gate, int k, int d, uint32_t* signs, void* stream) {
+  REQUIRE_PTR(w_gate);
+  REQUIRE_PTR(signs);
+  REQUIRE_ALIGNED(w_gate);
+  REQUIRE_ALIGNED(signs);
+  if (si_status s = check_kd(k, d)) return s;
+  return hip_status(si::launch_pack_signs_i8(w_gate, k, d, signs, (hipStream_t)stream), "pack_signs_i8 launch");
+}
+
+si_status si_transpose_down_i8(const int8_t* w_down, int d, int k, int8_t* w_down_t, void* stream) {
+  REQUIRE_PTR(w_down);
+  REQUIRE_PTR(w_down_t);
+  REQUIRE_ALIGNED(w_down);
+  REQUIRE_ALIGNED(w_down_t);
+  if (si_status s = check_kd(k, d)) return s;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(w_down), c = reinterpret_cast<uintptr_t>(w_down_t);
+  const uintptr_t n = (uintptr_t)k * (uintptr_t)d;
+  if (a < c + n && c < a + n) return fail(SI_ERR_SHAPE, "w_down and w_down_t overlap");
+  return hip_status(si::launch_transpose_i8(w_down, d, k, w_down_t, (hipStream_t)stream), "transpose_i8 launch");
+}
+
+si_status si_sparse_mlp_i8(const int8_t* w_gate, const float* s_gate, const int8_t* w_up, const float* s_up,
+                           const int8_t* w_down_t, const float* s_down, int k, int d, const uint16_t* x, int b,
+                           const uint8_t* mask, float* y, void* workspace, size_t workspace_bytes, uint32_t flags,
+                           int32_t* counters, void* stream) {
+  return int8_impl(false, nullptr, w_gate, s_gate, w_up, s_up, w_down_t, s_down, k, d, x, b, 0.0f, mask, nullptr,
+                   nullptr, nullptr, y, workspace, workspace_bytes, flags, counters, stream);
+}
+
+si_status si_predict_sparse_mlp_i8(const uint32_t* signs, const int8_t* w_gate, const float* s_gate,
+                                   const int8_t* w_up, const float* s_up, const int8_t* w_down_t,
+                                   const float* s_down, int k, int d, const uint16_t* x, int b, float alpha,
+                                   uint8_t* mask, int32_t* active_idx, int32_t* n_active, float* y,
+                                   void* workspace, size_t workspace_bytes, uint32_t flags, int32_t* counters,
+                                   void* stream) {
+  return int8_impl(true, signs, w_gate, s_gate, w_up, s_up, w_down_t, s_down, k, d, x, b, alpha, nullptr, mask,
+                   active_idx, n_active, y, workspace, workspace_bytes, flags, counters, stream);
+}
+
+}  // extern "C"

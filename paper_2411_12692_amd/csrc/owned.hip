@@ -32,6 +32,13 @@
 //               folded in LDS and the tile is added into y with fp32 atomics
 //               once the tile's owner has zeroed it in this call.
 //
+// INT8 weights (the kernel's third form): W_gate, W_up and W_down^T hold
+// INT8 values with one float scale per output channel (rows of W_gate and
+// W_up, columns of y for W_down^T).  The predictor reads the same packed
+// signs (the MSBs of the INT8 weights), gate/up converts each row's INT8
+// values exactly to fp16 in registers and scales the dot products, and the
+// down-projection scales each column of y once, at the tile's add.
+//
 // No block waits for the whole grid: the only exchanges are inside a group.
 // Block 0 adds the published kept counts (the count of the call) and, having
 // seen a word of this call from every block, advances the call counter.
@@ -84,6 +91,9 @@ struct OwnedArgs {
   const u32x4* wg;
   const u32x4* wu;         // nullptr: the non-gated ReLU MLP (h3 = ReLU(g))
   const u32x4* wdt;
+  const float* sg;         // INT8 form: scales of the rows of W_gate, W_up, and of the columns of y
+  const float* su;
+  const float* sd;
   const uint16_t* x;
   const uint8_t* mask_in;  // mask mode (else predict mode)
   int k, d, b, T, margin;
@@ -228,10 +238,94 @@ __device__ inline void row_dots2(const u32x4 (&v)[NU], const u32x4 (&w)[NU], con
   }
 }
 
-// BLOCK: the decoder-block form (x from the RMSNorm of h, y = h + MLP),
-// a separate instance so that the plain form carries none of its code (its
-// presence alone cost the plain form 0.3 us per call)
-template <int BM, int NU, bool BLOCK>
+// The 16 INT8 values of a 16-byte unit as 16 fp16 values (two 16-byte
+// vectors), exactly: each byte, offset by 128, becomes the low mantissa
+// byte of the fp16 value 1024 + (q + 128), from which 1152 is subtracted
+// (every value on the way is an integer below 2048).
+__device__ inline uint32_t i8_pair(uint32_t biased) {
+  return __builtin_bit_cast(uint32_t, as_h2(biased | 0x64006400u) - f16x2{(_Float16)1152.0f, (_Float16)1152.0f});
+}
+__device__ inline void i8_to_h16(u32x4 v, u32x4& lo, u32x4& hi) {
+  const uint32_t a = v.x ^ 0x80808080u, b = v.y ^ 0x80808080u, c = v.z ^ 0x80808080u, e = v.w ^ 0x80808080u;
+  auto p01 = [](uint32_t t) { return i8_pair((t & 0xffu) | ((t & 0xff00u) << 8)); };
+  auto p23 = [](uint32_t t) { return i8_pair(((t >> 16) & 0xffu) | ((t >> 8) & 0xff0000u)); };
+  lo = u32x4{p01(a), p23(a), p01(b), p23(b)};
+  hi = u32x4{p01(c), p23(c), p01(e), p23(e)};
+}
+
+// Dot products of one or two INT8 rows held as (NU + 1) / 2 16-byte units
+// per lane (unit lane + 64 j: 16 values, the tokens' fp16 units 2u and
+// 2u + 1) with the BM tokens in LDS; unscaled, wave-uniform results.
+template <int BM, int NU, bool TWO>
+__device__ inline void row_dots_i8(const u32x4 (&v)[(NU + 1) / 2], const u32x4 (&w)[(NU + 1) / 2],
+                                   const u32x4* xs, int U8, int lane, float (&o1)[BM], float (&o2)[BM]) {
+  constexpr int NU8 = (NU + 1) / 2;
+  float a1[BM], a2[BM];
+#pragma unroll
+  for (int t = 0; t < BM; ++t) a1[t] = a2[t] = 0.f;
+#pragma unroll
+  for (int j = 0; j < NU8; ++j) {
+    const int u = lane + kWave * j;
+    const int uc = min(u, U8 - 1);
+    u32x4 vl, vh, wl, wh;
+    i8_to_h16(v[j], vl, vh);
+    if constexpr (TWO) i8_to_h16(w[j], wl, wh);
+#pragma unroll
+    for (int t = 0; t < BM; ++t) {
+      const u32x4 x0 = xs[t * (NU * kWave) + 2 * uc], x1 = xs[t * (NU * kWave) + 2 * uc + 1];
+      const float s1 = dot8(vh, x1, dot8(vl, x0, a1[t]));
+      a1[t] = u < U8 ? s1 : a1[t];
+      if constexpr (TWO) {
+        const float s2 = dot8(wh, x1, dot8(wl, x0, a2[t]));
+        a2[t] = u < U8 ? s2 : a2[t];
+      }
+    }
+    if constexpr (BM >= 4) __builtin_amdgcn_sched_barrier(0);
+  }
+#pragma unroll
+  for (int t = 0; t < BM; ++t) {
+    o1[t] = wave_total(a1[t]);
+    o2[t] = TWO ? wave_total(a2[t]) : 0.f;
+  }
+}
+
+// A W_down^T piece of one row for one lane: 8 columns (fp16: 16 bytes; INT8:
+// 8 bytes) and their values as floats.
+template <bool I8>
+struct DownPiece {
+  typedef u32x4 type;
+  static __device__ inline type load(const u32x4* wdt, size_t row, int U, int unit) {
+    return load_nt(wdt + row * U + unit);
+  }
+  static __device__ inline void values(type v, float (&f)[8]) {
+    const f16x2 p0 = as_h2(v.x), p1 = as_h2(v.y), p2 = as_h2(v.z), p3 = as_h2(v.w);
+    f[0] = (float)p0.x; f[1] = (float)p0.y; f[2] = (float)p1.x; f[3] = (float)p1.y;
+    f[4] = (float)p2.x; f[5] = (float)p2.y; f[6] = (float)p3.x; f[7] = (float)p3.y;
+  }
+};
+template <>
+struct DownPiece<true> {
+  typedef uint32_t type __attribute__((ext_vector_type(2)));
+  static __device__ inline type load(const u32x4* wdt, size_t row, int U, int unit) {
+    return __builtin_nontemporal_load(reinterpret_cast<const type*>(wdt) + row * U + unit);
+  }
+  static __device__ inline void values(type v, float (&f)[8]) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      f[i] = (float)(int8_t)(v.x >> (8 * i));
+      f[4 + i] = (float)(int8_t)(v.y >> (8 * i));
+    }
+  }
+};
+
+constexpr int kModePlain = 0;  // fp16 weights, x given
+constexpr int kModeBlock = 1;  // fp16 weights, x = RMSNorm(h) * norm_w, y = h + MLP
+constexpr int kModeInt8 = 2;   // INT8 weights with per-channel scales, x given
+
+// MODE: the kernel's form (above); each is a separate instance so that the
+// plain form carries none of the others' code (the decoder-block code alone
+// cost the plain form 0.3 us per call)
+template <int BM, int NU, int MODE>
 __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
   OwnedLds<BM, NU>& L = *reinterpret_cast<OwnedLds<BM, NU>*>(lds_raw);
@@ -280,7 +374,8 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   // the owner of tile blk of y zeroes it (in decoder-block mode it copies
   // the residual in later); the same wave later announces it in the tile's
   // flag
-  constexpr bool block_mode = BLOCK;
+  constexpr bool block_mode = MODE == kModeBlock;
+  constexpr bool kI8 = MODE == kModeInt8;
   if (!block_mode && owns_tile && wv == kTileWave) {
     const int half_cols = min(kTile, d - blk * kTile) / 2;
     for (int t = 0; t < b; ++t) {
@@ -591,7 +686,50 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       float g[BM], u[BM];
       bool up;
       // a row's requests and their use sit in one branch (row-uniform)
-      if (gated && ((spec_ok && (e >> 31)) || no_as)) {
+      if constexpr (kI8) {
+        // INT8 rows: U8 = d / 16 units of 16 values; scales read as the row's
+        // requests go out, applied to the dot products
+        constexpr int NU8 = (NU + 1) / 2;
+        const int U8 = d >> 4;
+        const uint32_t urow = uniform(row);
+        if (gated && ((spec_ok && (e >> 31)) || no_as)) {
+          u32x4 vg[NU8], vu[NU8];
+          load_row<NU8>(a.wg + (size_t)urow * U8, U8, lane, vg);
+          load_row<NU8>(a.wu + (size_t)urow * U8, U8, lane, vu);
+          const float sgv = a.sg[urow], suv = a.su[urow];
+          row_dots_i8<BM, NU, true>(vg, vu, L.xs, U8, lane, g, u);
+#pragma unroll
+          for (int t = 0; t < BM; ++t) {
+            g[t] *= sgv;
+            u[t] *= suv;
+          }
+          up = true;
+        } else {
+          u32x4 vg[NU8];
+          load_row<NU8>(a.wg + (size_t)urow * U8, U8, lane, vg);
+          const float sgv = a.sg[urow];
+          row_dots_i8<BM, NU, false>(vg, vg, L.xs, U8, lane, g, u);
+          bool any = false;
+#pragma unroll
+          for (int t = 0; t < BM; ++t) {
+            g[t] *= sgv;
+            any |= g[t] > 0.f;
+          }
+          up = gated && any;
+          if (up) {
+            u32x4 vu[NU8];
+            load_row<NU8>(a.wu + (size_t)urow * U8, U8, lane, vu);
+            const float suv = a.su[urow];
+            float unused[BM];
+            row_dots_i8<BM, NU, false>(vu, vu, L.xs, U8, lane, u, unused);
+#pragma unroll
+            for (int t = 0; t < BM; ++t) u[t] *= suv;
+          } else {
+#pragma unroll
+            for (int t = 0; t < BM; ++t) u[t] = gated ? 0.f : 1.f;
+          }
+        }
+      } else if (gated && ((spec_ok && (e >> 31)) || no_as)) {
         u32x4 vg[NU], vu[NU];
         load_row<NU>(a.wg + (size_t)row * U, U, lane, vg);
         load_row<NU>(a.wu + (size_t)row * U, U, lane, vu);
@@ -641,17 +779,18 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     const int dunit = tile * kWave + lane;
     const bool dcol_ok = dunit < U;
     constexpr bool kZLane = kODN * BM < kWave;  // wave 0's lane 63 is free for the zero flag
+    typedef DownPiece<kI8> DP;
     for (int q0 = 0; q0 < dN; q0 += kODownRound) {
-      u32x4 vd[kODN];
+      typename DP::type vd[kODN];
       uint32_t dl = 0;
 #pragma unroll
       for (int j = 0; j < kODN; ++j) {
-        vd[j] = u32x4{0, 0, 0, 0};
+        vd[j] = typename DP::type{};
         const int q = q0 + wv + kOW * j;
         if (q < dN) {
           const uint32_t e = L.dent[q];
           if ((spec_ok && (e >> 31)) || no_as) {
-            if (dcol_ok) vd[j] = load_nt(a.wdt + (size_t)(e & 0x7fffffffu) * U + dunit);
+            if (dcol_ok) vd[j] = DP::load(a.wdt, e & 0x7fffffffu, U, dunit);
             dl |= 1u << j;
           }
         }
@@ -681,12 +820,11 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         }
         if (q < dN && !((dl >> j) & 1u) && nz) {  // late request
           const uint32_t e = L.dent[q];
-          if (dcol_ok) vd[j] = load_nt(a.wdt + (size_t)(e & 0x7fffffffu) * U + dunit);
+          if (dcol_ok) vd[j] = DP::load(a.wdt, e & 0x7fffffffu, U, dunit);
           dl |= 1u << j;
         }
-        const f16x2 p0 = as_h2(vd[j].x), p1 = as_h2(vd[j].y), p2 = as_h2(vd[j].z), p3 = as_h2(vd[j].w);
-        const float f[8] = {(float)p0.x, (float)p0.y, (float)p1.x, (float)p1.y,
-                            (float)p2.x, (float)p2.y, (float)p3.x, (float)p3.y};
+        float f[8];
+        DP::values(vd[j], f);
 #pragma unroll
         for (int t = 0; t < BM; ++t)
 #pragma unroll
@@ -739,7 +877,11 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         float v = 0.f;
 #pragma unroll
         for (int s2 = 0; s2 < kFold; ++s2) v += L.dpart[s2][t][c];
-        if (col < d && v != 0.f) unsafeAtomicAdd(&a.y[(size_t)t * d + col], v);
+        if constexpr (kI8) {
+          if (col < d && v != 0.f) unsafeAtomicAdd(&a.y[(size_t)t * d + col], v * a.sd[col]);
+        } else {
+          if (col < d && v != 0.f) unsafeAtomicAdd(&a.y[(size_t)t * d + col], v);
+        }
       }
     }
     if (tid == 0) {
@@ -780,7 +922,7 @@ static int owned_rows_per_block(int k, int P, int tiles) {
   return (R + 7) / 8 * 8;
 }
 
-template <int BM, int NU, bool BLOCK = false>
+template <int BM, int NU, int MODE = kModePlain>
 static int owned_blocks() {
   static int blocks = -1;
   if (blocks < 0) {
@@ -788,7 +930,7 @@ static int owned_blocks() {
     constexpr int lds = owned_lds_bytes<BM, NU>();
     if constexpr (lds <= kMaxLds) {
       int dev = 0, cus = 0, per_cu = 0;
-      const void* fn = reinterpret_cast<const void*>(&k_owned<BM, NU, BLOCK>);
+      const void* fn = reinterpret_cast<const void*>(&k_owned<BM, NU, MODE>);
       if (hipGetDevice(&dev) != hipSuccess) return 0;
       if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
       if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return 0;
@@ -807,14 +949,19 @@ static hipError_t owned_b(const LayerCall& c, hipStream_t s) {
     const int k = c.k, d = c.d;
     const WsLayout L = ws_layout(k, c.b);
     char* base = static_cast<char*>(c.ws);
-    const bool block = c.h != nullptr;
-    const int P = block ? owned_blocks<BM, NU, true>() : owned_blocks<BM, NU, false>();
+    const int mode = c.i8 ? kModeInt8 : c.h != nullptr ? kModeBlock : kModePlain;
+    const int P = mode == kModeInt8    ? owned_blocks<BM, NU, kModeInt8>()
+                  : mode == kModeBlock ? owned_blocks<BM, NU, kModeBlock>()
+                                       : owned_blocks<BM, NU, kModePlain>();
     if (P < 1) return hipErrorInvalidConfiguration;
     OwnedArgs a;
     a.signs = reinterpret_cast<const u32x4*>(c.signs);
     a.wg = reinterpret_cast<const u32x4*>(c.w_gate);
     a.wu = reinterpret_cast<const u32x4*>(c.w_up);
     a.wdt = reinterpret_cast<const u32x4*>(c.w_down_t);
+    a.sg = c.s_gate;
+    a.su = c.s_up;
+    a.sd = c.s_down;
     a.x = c.x;
     a.mask_in = c.mask_in;
     a.k = k;
@@ -840,10 +987,12 @@ static hipError_t owned_b(const LayerCall& c, hipStream_t s) {
     a.h = c.h;
     a.norm_w = c.norm_w;
     a.eps = c.eps;
-    if (block)
-      k_owned<BM, NU, true><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
+    if (mode == kModeInt8)
+      k_owned<BM, NU, kModeInt8><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
+    else if (mode == kModeBlock)
+      k_owned<BM, NU, kModeBlock><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
     else
-      k_owned<BM, NU, false><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
+      k_owned<BM, NU, kModePlain><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !c.counters || !c.y) return e;
     return launch_sum_counts(a.counts, P, c.n_out, k, c.counters, s);

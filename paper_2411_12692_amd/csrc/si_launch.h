@@ -10,6 +10,9 @@ namespace si {
 hipError_t launch_pack_signs(const uint16_t* w_gate, int k, int d, uint32_t* signs, hipStream_t s);
 hipError_t launch_signs_to_canonical(const uint32_t* signs, int k, int d, uint32_t* out, hipStream_t s);
 hipError_t launch_transpose(const uint16_t* in, int rows, int cols, uint16_t* out, hipStream_t s);
+hipError_t launch_transpose_i8(const int8_t* in, int rows, int cols, int8_t* out, hipStream_t s);
+hipError_t launch_pack_signs_i8(const int8_t* w_gate, int k, int d, uint32_t* signs, hipStream_t s);
+hipError_t launch_quantize_rows(const uint16_t* w, int rows, int n, int8_t* q, float* scale, hipStream_t s);
 
 // Predictor: x-sign pack, XOR/popcount, Eq. (2) via threshold T, mask and
 // ordered compaction.  `ws` is the workspace base.
@@ -55,6 +58,12 @@ struct LayerCall {
   const float* h = nullptr;
   const float* norm_w = nullptr;
   float eps = 0.f;
+  // INT8 form (row-owning kernel only): w_gate, w_up and w_down_t hold INT8
+  // values with scales per row of W_gate / W_up and per column of y
+  bool i8 = false;
+  const float* s_gate = nullptr;
+  const float* s_up = nullptr;
+  const float* s_down = nullptr;
 };
 bool layer_supported(int k, int d, int b);
 hipError_t launch_layer(const LayerCall& c, hipStream_t s);
