@@ -16,6 +16,13 @@ Steps cycle through a pool of independently seeded layers whose weights
 from HBM.  The timed loop is replayed from a HIP graph (the per-call host
 cost of Python would otherwise dominate a ~10 us step).
 
+``--report alpha|stacks|sweep`` prints the other measurements of the
+workloads instead, one JSON line per point: the alpha sweep of the 7B layer
+(time, bytes, recall, speedup over the dense call), the 32-layer 7B and
+40-layer 13B decode stacks (us per layer and tokens/s, chained through the
+stacks' glue, plus the predictor alone), and the sparsity x batch sweep
+(sparse against dense calls at the same batch, and where dense wins).
+
 Prints one JSON line.  ``value`` is the effective HBM bandwidth on the
 algorithmic bytes of a step (packed signs + x + the kept rows of W_gate,
 W_up and W_down^T + y), divided by the measured time per step.
@@ -105,6 +112,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--launches", type=int, default=256, help="individually timed launches for the roofline")
+    ap.add_argument("--report", choices=("alpha", "stacks", "sweep"), default=None,
+                    help="alpha: the alpha sweep of the 7B layer; stacks: the 7B and 13B decode stacks; sweep: "
+                         "sparsity x batch against dense (JSON line per point; no headline line)")
+    ap.add_argument("--tokens", type=int, default=256, help="decode steps of --report stacks")
     ap.add_argument("--profile-pass", action="store_true",
                     help="for hardware-counter runs: eager layer calls over the pool, then one plain 256 MiB "
                          "device copy whose counters calibrate the byte counters; prints no JSON")
@@ -215,6 +226,283 @@ def time_graph(step, n_layers, steps_wanted, warmup_wanted):
     return e0.elapsed_time(e1) * 1e3 / steps, steps, warmup, wall * 1e6 / steps
 
 
+def graph_us(fn, calls, reps=4, warm=1):
+    """Average us per call of ``fn(i)`` for i < calls, replayed from a HIP
+    graph ``reps`` times after ``warm`` untimed replays (events on the replay
+    stream)."""
+    import torch
+
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        for i in range(min(calls, 16)):
+            fn(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for i in range(calls):
+            fn(i)
+    for _ in range(warm):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(reps):
+            g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    del g
+    return e0.elapsed_time(e1) * 1e3 / (reps * calls)
+
+
+def dense_torch_mlp(wg, wu, wd, x):
+    """The dense gated MLP through torch's fp16 GEMMs (the vendor library),
+    for reference only: ReLU(x W_gate^T) * (x W_up^T) W_down^T."""
+    import torch.nn.functional as F
+
+    return F.linear(F.relu(F.linear(x, wg)) * F.linear(x, wu), wd)
+
+
+def report_alpha(args, si, synth, dev):
+    """The 7B workload's alpha sweep: per alpha, us per fused call, kept
+    rows, algorithmic bytes and GB/s, active recall and the paper's
+    precision / recall of the predicted-sparse class (truth: which gate
+    pre-activations are positive, from a dense fp32 product on the device),
+    and the speedup over the same call at alpha = +inf (every row kept) and
+    over torch's dense fp16 GEMMs."""
+    import torch
+
+    from paper_2411_12692_amd import schedule
+
+    L = args.layers
+    pls = [synth.planted_layer(D, K, S, config=2, layer=l, device=dev) for l in range(L)]
+    layers = [si.MLPLayer(p.w_gate, p.w_up, p.w_down, keep_w_down=True) for p in pls]
+    xs = [p.x for p in pls]
+    pos = [schedule.gate_positive(p.w_gate, p.x) for p in pls]
+    del pls
+    ys = [torch.empty(1, D, dtype=torch.float32, device=dev) for _ in range(L)]
+    dense_torch = graph_us(lambda i: dense_torch_mlp(layers[i % L].w_gate, layers[i % L].w_up,
+                                                     layers[i % L].w_down, xs[i % L]), 4 * L)
+    rows = []
+    for alpha in (0.7, 1.0, 1.03, 1.45, 1.5, math.inf):
+        kept, q = [], []
+        bsum = 0
+        for l in range(L):
+            _, (mask, _, _, cnt) = layers[l](xs[l], alpha, outputs=True)
+            c = cnt.tolist()
+            bsum += algorithmic_bytes(K, D, 1, *c)
+            kept.append(c[0])
+            q.append(schedule.quality(mask, pos[l]))
+        us = graph_us(lambda i: layers[i % L](xs[i % L], alpha, y=ys[i % L]), 4 * L, reps=16)
+        rows.append({"alpha": alpha, "us_per_layer": round(us, 3), "kept_rows_mean": sum(kept) / L,
+                     "bytes_per_layer": int(bsum / L), "gbs": round(bsum / L / us / 1e3, 1),
+                     "frac_of_peak": round(bsum / L / us / 1e3 / HBM_PEAK_GBS, 4),
+                     "active_recall": round(sum(x["active_recall"] for x in q) / L, 5),
+                     "missed_rows_total": sum(x["missed"] for x in q),
+                     "sparse_precision": round(sum(x["sparse_precision"] for x in q) / L, 5),
+                     "sparse_recall": round(sum(x["sparse_recall"] for x in q) / L, 5)})
+    dense = rows[-1]["us_per_layer"]
+    for r in rows:
+        r["speedup_vs_dense_call"] = round(dense / r["us_per_layer"], 2)
+        r["speedup_vs_torch_dense"] = round(dense_torch / r["us_per_layer"], 2)
+        r.update({"report": "alpha", "workload": f"7B-shaped layer d={D} k={K}, planted s={S}, batch 1, pool of {L}",
+                  "torch_dense_us": round(dense_torch, 3)})
+        print(json.dumps(r), flush=True)
+
+
+def report_stacks(args, si, synth, dev):
+    """The decode stacks: 32 layers of the 7B shape with per-layer planted
+    sparsity from U(0.85, 0.95) and 40 layers of the 13B shape at 0.88,
+    alpha = 1, batch 1.  Each token runs every layer in order, the input of
+    a layer made from the previous layer's output and fresh noise
+    (``synth.stack_glue``, elementwise torch work); the whole token is
+    replayed from one graph with the noise of each token gathered from a
+    precomputed buffer.  Reported: us per token with and without the glue
+    (the glue replayed alone), us per layer, tokens/s, bytes and GB/s; the
+    fused call alone over the stack's layers (fixed inputs); the predictor
+    alone (``si_predict``); the CPU oracle on layers {first, middle, last}
+    x tokens {0, 1} with the inputs the GPU path received."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    T = args.tokens
+    for name, d, k, n_layers, (lo, hi), config in (("7b", 4096, 11008, 32, (0.85, 0.95), 3),
+                                                    ("13b", 5120, 13824, 40, (0.88, 0.88), 4)):
+        sp = synth.stack_sparsities(n_layers, lo, hi, config)
+        sample = sorted({0, n_layers // 2, n_layers - 1})  # layers of the CPU-oracle sample
+        layers, negs, noise = [], [], []
+        for l in range(n_layers):
+            wg, wu, wd, _, ref = synth.stack_layer(d, k, sp[l], config, l, dev)
+            layers.append(si.MLPLayer(wg, wu, wd, keep_w_down=l in sample))
+            del wd
+            negs.append(ref)
+            noise.append(torch.cat([synth.stack_noise(d, 1, config, l, t, dev) for t in range(T)]))
+        ys = [torch.empty(1, d, dtype=torch.float32, device=dev) for _ in range(n_layers)]
+        # device-side token counter (gathers each token's noise inside the
+        # graph); `issued` shadows it on the host so that no gather can go
+        # past the T precomputed rows
+        tok = torch.zeros(1, dtype=torch.long, device=dev)
+        issued = [0]
+        print(f"# {name} stack of {n_layers} layers ready", file=sys.stderr, flush=True)
+
+        def reset():
+            tok.zero_()
+            issued[0] = 0
+
+        def token(mlp=True, count=True, keep=None):
+            if count:
+                assert issued[0] < T, "token counter past the precomputed noise"
+                issued[0] += 1
+            y_prev = None
+            for l in range(n_layers):
+                x = synth.stack_glue(y_prev, noise[l].index_select(0, tok), negs[l])
+                if keep is not None:
+                    keep.append(x)
+                if mlp:
+                    layers[l](x, 1.0, y=ys[l])
+                y_prev = ys[l]
+            tok.add_(1)
+
+        # eager: the first two tokens, keeping every layer's input (for the
+        # oracle sample and the fixed-input timing)
+        inputs = []
+        reset()
+        for t in range(2):
+            keep = []
+            token(keep=keep)
+            inputs.append(keep)
+        xs0 = [x.clone() for x in inputs[0]]
+        counts = []
+        for l in range(n_layers):
+            _, (_, _, _, c) = layers[l](xs0[l], 1.0, outputs=True)
+            counts.append(c)
+        torch.cuda.synchronize()
+        counts = [c.tolist() for c in counts]
+        bytes_token = sum(algorithmic_bytes(k, d, 1, *c) for c in counts)
+
+        def timed_tokens(mlp):
+            stream = torch.cuda.Stream()
+            g = torch.cuda.CUDAGraph()
+            reset()
+            with torch.cuda.stream(stream):
+                token(mlp)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(g, stream=stream):
+                token(mlp, count=False)  # captured, not run
+            reset()
+            issued[0] += 1
+            g.replay()
+            reset()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0 = time.perf_counter()
+            e0.record(stream)
+            with torch.cuda.stream(stream):
+                for _ in range(T):
+                    assert issued[0] < T
+                    issued[0] += 1
+                    g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - t0
+            reset()
+            del g
+            return e0.elapsed_time(e1) * 1e3 / T, wall * 1e6 / T
+
+        total_us, wall_us = timed_tokens(True)
+        glue_us, _ = timed_tokens(False)
+        fixed_us = graph_us(lambda i: layers[i % n_layers](xs0[i % n_layers], 1.0, y=ys[i % n_layers]),
+                            n_layers * max(1, 64 // n_layers), reps=8)
+        pred_us = graph_us(lambda i: layers[i % n_layers].predict(xs0[i % n_layers], 1.0),
+                           n_layers * max(1, 64 // n_layers), reps=8)
+        mlp_token_us = total_us - glue_us
+        # eager tokens (Python issues every call)
+        reset()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(8):
+            token()
+        torch.cuda.synchronize()
+        eager_us = (time.perf_counter() - t0) * 1e6 / 8
+        reset()
+        row = {
+            "report": "stacks", "stack": name,
+            "workload": f"{n_layers} layers d={d} k={k}, planted s~U({lo},{hi}) per layer, alpha=1, batch 1, "
+                        f"{T} decode tokens chained through the stack's glue",
+            "kept_rows_per_layer_mean": round(sum(c[0] for c in counts) / n_layers, 1),
+            "bytes_per_token": int(bytes_token),
+            "us_per_token_total": round(total_us, 2), "us_per_token_glue": round(glue_us, 2),
+            "us_per_token_mlp": round(mlp_token_us, 2),
+            "us_per_layer": round(mlp_token_us / n_layers, 3),
+            "tokens_per_s_mlp": round(1e6 / mlp_token_us, 1),
+            "tokens_per_s_with_glue": round(1e6 / total_us, 1),
+            "wall_us_per_token": round(wall_us, 2),
+            "eager_us_per_token": round(eager_us, 1),
+            "gbs": round(bytes_token / mlp_token_us / 1e3, 1),
+            "frac_of_peak": round(bytes_token / mlp_token_us / 1e3 / HBM_PEAK_GBS, 4),
+            "fixed_input_us_per_layer": round(fixed_us, 3),
+            "predict_only_us_per_layer": round(pred_us, 3),
+        }
+        if not args.no_cpu_baseline:
+            def u16(t):
+                return t.detach().cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+            secs, n = 0.0, 0
+            for l in sample:
+                wg = u16(layers[l].w_gate)
+                wu = u16(layers[l].w_up)
+                wd = u16(layers[l].w_down)
+                packed = oracle.pack_signs(wg)
+                for t in range(2):
+                    x = u16(inputs[t][l])
+                    t0 = time.perf_counter()
+                    mask = oracle.predict_rows(packed, x, 1.0)[0]
+                    oracle.sparse_mlp(wg, wu, wd, x, mask)
+                    secs += time.perf_counter() - t0
+                    n += 1
+            row["cpu_baseline"] = {"us_per_layer": round(secs / n * 1e6, 1), "cores": 1, "kind": "oracle",
+                                   "sample": f"layers first/middle/last x tokens 0, 1 ({n} calls, the GPU path's "
+                                             f"inputs, predict_rows + sparse_mlp, numpy float64)"}
+        print(json.dumps(row), flush=True)
+        del layers, noise, inputs, xs0
+        torch.cuda.empty_cache()
+
+
+def report_sweep(args, si, synth, dev):
+    """Sparsity x batch at the 7B shape: per planted s and batch b, the
+    union of b per-token active sets (``synth.batch_union_mask``) through
+    ``si_sparse_mlp`` in mask mode, against the same call with every row
+    kept (the dense call) and torch's dense fp16 GEMMs at the same b."""
+    import torch
+
+    L = 8
+    for s_ in (0.5, 0.7, 0.8, 0.9, 0.95, 0.97):
+        pls = [synth.planted_layer(D, K, s_, config=5, layer=l, device=dev) for l in range(L)]
+        layers = [si.MLPLayer(p.w_gate, p.w_up, p.w_down, max_batch=8, keep_w_down=True) for p in pls]
+        ones = torch.ones(K, dtype=torch.uint8, device=dev)
+        for b in (1, 2, 4, 8):
+            xs = [synth.batch_tokens(p, b, config=5, layer_id=l) for l, p in enumerate(pls)]
+            ms = [synth.batch_union_mask(p, b, config=5, layer_id=l) for l, p in enumerate(pls)]
+            cnts = [layers[l].sparse_mlp(xs[l], mask=ms[l], counters=True)[1] for l in range(L)]
+            torch.cuda.synchronize()
+            bsum = sum(algorithmic_bytes(K, D, b, *c.tolist()) for c in cnts)
+            sp = graph_us(lambda i: layers[i % L].sparse_mlp(xs[i % L], mask=ms[i % L]), 4 * L, reps=8)
+            dn = graph_us(lambda i: layers[i % L].sparse_mlp(xs[i % L], mask=ones), 4 * L, reps=8)
+            tdn = graph_us(lambda i: dense_torch_mlp(layers[i % L].w_gate, layers[i % L].w_up, layers[i % L].w_down,
+                                                     xs[i % L]), 4 * L, reps=8)
+            rows = sum(int(m.sum()) for m in ms) / L
+            print(json.dumps({
+                "report": "sweep", "s": s_, "b": b, "union_rows_mean": rows, "union_density": round(rows / K, 4),
+                "sparse_us": round(sp, 3), "dense_call_us": round(dn, 3), "torch_dense_us": round(tdn, 3),
+                "speedup_vs_dense_call": round(dn / sp, 2), "speedup_vs_torch_dense": round(tdn / sp, 2),
+                "sparse_gbs": round(bsum / L / sp / 1e3, 1), "dense_wins": sp > dn,
+                "workload": f"7B-shaped layer d={D} k={K}, union masks of {b} per-token planted sets, pool of {L}",
+            }), flush=True)
+        del layers, pls
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -236,6 +524,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     si._lib.load()  # fails loudly if the library is not built
+    if args.report:
+        {"alpha": report_alpha, "stacks": report_stacks, "sweep": report_sweep}[args.report](args, si, synth, dev)
+        return
 
     relu = args.mlp == "relu"
     block = args.mlp == "block"

@@ -59,9 +59,8 @@ def fp16_with_sign(magnitude: torch.Tensor, negative: torch.Tensor) -> torch.Ten
     from ``negative`` (set on the bit pattern, so -0.0 is produced where the
     magnitude rounds to zero)."""
     m = magnitude.abs().to(torch.float16).view(torch.int16)
-    m = m & torch.tensor(0x7FFF, dtype=torch.int16, device=m.device)
-    sign = torch.tensor(-32768, dtype=torch.int16, device=m.device)  # 0x8000
-    return torch.where(negative, m | sign, m).view(torch.float16)
+    m = m & 0x7FFF  # Python scalars keep int16 and need no host-to-device copy (graph capture)
+    return torch.where(negative, m | -32768, m).view(torch.float16)  # -32768: the 0x8000 sign bit
 
 
 @dataclass
@@ -191,14 +190,23 @@ def stack_input(y_prev, d: int, b: int, config: int, layer: int, token: int, dev
     This is harness glue between stacked MLP blocks, not part of the method.
     """
     eps = stack_noise(d, b, config, layer, token, device)
+    return stack_glue(y_prev, eps, reference_signs(d, config, layer, device))
+
+
+def stack_glue(y_prev, eps: torch.Tensor, negative: torch.Tensor) -> torch.Tensor:
+    """The chaining of :func:`stack_input` from its random draws: ``eps``
+    ``[b][d]`` float32 noise and the layer's reference signs ``negative``
+    (``[d]`` bool).  Only elementwise torch operations, so a benchmark can
+    replay it from a graph with the noise of each token gathered from a
+    precomputed buffer."""
+    b, d = eps.shape
     if y_prev is None:
         mag = eps.abs()
     else:
         y = y_prev.float().reshape(b, d)
         rms = y.pow(2).mean(dim=-1, keepdim=True).sqrt().clamp_min(1e-30)
         mag = (y / rms + eps).abs()
-    neg = reference_signs(d, config, layer, device)
-    return fp16_with_sign(mag, neg[None, :].expand(b, d))
+    return fp16_with_sign(mag, negative[None, :].expand(b, d))
 
 
 def calibration_tokens(d: int, n: int, config: int, layer: int, flip: float = 0.0, device="cpu") -> torch.Tensor:
