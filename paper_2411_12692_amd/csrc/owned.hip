@@ -685,6 +685,12 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       const uint32_t row = e & 0x7fffffffu;
       float g[BM], u[BM];
       bool up;
+      // with 4 or 8 tokens the per-lane unit addresses of the row loads and
+      // token reads are formed again in every iteration (a few integer
+      // operations) rather than kept live across the loop, where they were
+      // spilled to scratch memory and read back in every iteration
+      int ln = lane;
+      if constexpr (BM >= 4) asm volatile("" : "+v"(ln));
       // a row's requests and their use sit in one branch (row-uniform)
       if constexpr (kI8) {
         // INT8 rows: U8 = d / 16 units of 16 values; scales read as the row's
@@ -694,10 +700,10 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         const uint32_t urow = uniform(row);
         if (gated && ((spec_ok && (e >> 31)) || no_as)) {
           u32x4 vg[NU8], vu[NU8];
-          load_row<NU8>(a.wg + (size_t)urow * U8, U8, lane, vg);
-          load_row<NU8>(a.wu + (size_t)urow * U8, U8, lane, vu);
+          load_row<NU8>(a.wg + (size_t)urow * U8, U8, ln, vg);
+          load_row<NU8>(a.wu + (size_t)urow * U8, U8, ln, vu);
           const float sgv = a.sg[urow], suv = a.su[urow];
-          row_dots_i8<BM, NU, true>(vg, vu, L.xs, U8, lane, g, u);
+          row_dots_i8<BM, NU, true>(vg, vu, L.xs, U8, ln, g, u);
 #pragma unroll
           for (int t = 0; t < BM; ++t) {
             g[t] *= sgv;
@@ -706,9 +712,9 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
           up = true;
         } else {
           u32x4 vg[NU8];
-          load_row<NU8>(a.wg + (size_t)urow * U8, U8, lane, vg);
+          load_row<NU8>(a.wg + (size_t)urow * U8, U8, ln, vg);
           const float sgv = a.sg[urow];
-          row_dots_i8<BM, NU, false>(vg, vg, L.xs, U8, lane, g, u);
+          row_dots_i8<BM, NU, false>(vg, vg, L.xs, U8, ln, g, u);
           bool any = false;
 #pragma unroll
           for (int t = 0; t < BM; ++t) {
@@ -718,10 +724,11 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
           up = gated && any;
           if (up) {
             u32x4 vu[NU8];
-            load_row<NU8>(a.wu + (size_t)urow * U8, U8, lane, vu);
+            load_row<NU8>(a.wu + (size_t)urow * U8, U8, ln, vu);
+            if constexpr (BM >= 2) asm volatile("" ::: "memory");
             const float suv = a.su[urow];
             float unused[BM];
-            row_dots_i8<BM, NU, false>(vu, vu, L.xs, U8, lane, u, unused);
+            row_dots_i8<BM, NU, false>(vu, vu, L.xs, U8, ln, u, unused);
 #pragma unroll
             for (int t = 0; t < BM; ++t) u[t] *= suv;
           } else {
@@ -731,23 +738,26 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         }
       } else if (gated && ((spec_ok && (e >> 31)) || no_as)) {
         u32x4 vg[NU], vu[NU];
-        load_row<NU>(a.wg + (size_t)row * U, U, lane, vg);
-        load_row<NU>(a.wu + (size_t)row * U, U, lane, vu);
+        load_row<NU>(a.wg + (size_t)row * U, U, ln, vg);
+        load_row<NU>(a.wu + (size_t)row * U, U, ln, vu);
         SI_TRACE_WAVE(0);
-        row_dots2<BM, NU>(vg, vu, L.xs, U, lane, g, u);
+        row_dots2<BM, NU>(vg, vu, L.xs, U, ln, g, u);
         up = true;
       } else {
         u32x4 vg[NU];
-        load_row<NU>(a.wg + (size_t)row * U, U, lane, vg);
-        row_dots<BM, NU>(vg, L.xs, U, lane, g);
+        load_row<NU>(a.wg + (size_t)row * U, U, ln, vg);
+        row_dots<BM, NU>(vg, L.xs, U, ln, g);
         bool any = false;
 #pragma unroll
         for (int t = 0; t < BM; ++t) any |= g[t] > 0.f;
         up = gated && any;
         if (up) {
           u32x4 vu[NU];
-          load_row<NU>(a.wu + (size_t)row * U, U, lane, vu);
-          row_dots<BM, NU>(vu, L.xs, U, lane, u);
+          load_row<NU>(a.wu + (size_t)row * U, U, ln, vu);
+          // the tokens are read from LDS again: kept from the gate products,
+          // 2..8 tokens' units would not fit in registers and were spilled
+          if constexpr (BM >= 2) asm volatile("" ::: "memory");
+          row_dots<BM, NU>(vu, L.xs, U, ln, u);
         } else {  // h3 = ReLU(g) * 1 without W_up
 #pragma unroll
           for (int t = 0; t < BM; ++t) u[t] = gated ? 0.f : 1.f;
