@@ -139,20 +139,16 @@ def profile_pass(step, n_layers, calls, dev):
     print(f"# profile pass: {calls} layer calls, 4 copies of {src.numel() * 2} bytes", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None, int8=False):
-    """Time the CPU oracle (test infrastructure, never tuned) on a bounded
-    sample of the same workload: predict + masked MLP on the first layers of
-    the pool, repeated until the budget is spent, with one BLAS thread
-    (``wu is None``: the non-gated MLP; ``block`` = per-layer ``(h, norm_w,
-    eps)``: the decoder-block form, RMSNorm and residual included; ``int8``:
-    the entries hold the oracle's INT8 weights and scales, quantized beforehand,
-    untimed, as at load)."""
-    from threadpoolctl import threadpool_limits
+def _oracle_pass(layers_host, alpha, budget_s, k, d, block, int8, threads):
+    """Oracle calls over the host layers until ``budget_s`` seconds of them
+    have run, with ``threads`` BLAS threads: (bytes, seconds, calls)."""
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     import oracle
 
     total_bytes, total_s, calls = 0.0, 0.0, 0
-    with threadpool_limits(limits=1):
+    with threadpool_limits(limits=threads):
+        used = max([p["num_threads"] for p in threadpool_info() if p["user_api"] == "blas"] or [1])
         while total_s < budget_s:
             for li, (wg, wu, wd, x, packed) in enumerate(layers_host):
                 t0 = time.perf_counter()
@@ -175,6 +171,21 @@ def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None, int8=False)
                                                  block=block is not None, int8=int8)
                 if total_s >= budget_s:
                     break
+    return total_bytes, total_s, calls, used
+
+
+def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None, int8=False):
+    """Time the CPU oracle (test infrastructure, never tuned) on a bounded
+    sample of the same workload: predict + masked MLP on the first layers of
+    the pool, repeated until the budget is spent, with one BLAS thread, then
+    for half that budget with as many BLAS threads as the process may use
+    (``wu is None``: the non-gated MLP; ``block`` = per-layer ``(h, norm_w,
+    eps)``: the decoder-block form, RMSNorm and residual included; ``int8``:
+    the entries hold the oracle's INT8 weights and scales, quantized
+    beforehand, untimed, as at load)."""
+    total_bytes, total_s, calls, _ = _oracle_pass(layers_host, alpha, budget_s, k, d, block, int8, 1)
+    ncores = len(os.sched_getaffinity(0))
+    mt_bytes, mt_s, mt_calls, mt_threads = _oracle_pass(layers_host, alpha, budget_s / 2, k, d, block, int8, ncores)
     what = ("rmsnorm_fp16 + predict_rows + sparse_mlp + residual" if block is not None else
             "predict_rows on pack_signs_int8 + int8_mlp" if int8 else
             f"predict_rows + {'relu_mlp' if layers_host[0][1] is None else 'sparse_mlp'}")
@@ -187,6 +198,11 @@ def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None, int8=False)
         "sample": f"{calls} layer calls over the first {len(layers_host)} layers of the pool "
                   f"({what}, numpy float64, 1 thread, {total_s:.1f} s)",
         "cpu": platform.processor() or platform.machine(),
+        "all_cores": {"value": round(mt_bytes / mt_s / 1e9, 3), "unit": "GB/s",
+                      "us_per_layer": round(mt_s / mt_calls * 1e6, 1), "threads": mt_threads,
+                      "affinity_cores": ncores, "os_cpu_count": os.cpu_count(),
+                      "sample": f"{mt_calls} layer calls, the same sample with {mt_threads} BLAS threads "
+                                f"({mt_s:.1f} s)"},
     }
 
 
