@@ -387,15 +387,21 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   constexpr int XS = OwnedLds<BM, NU>::kUnits;
   // decoder-block mode: h and norm_w as 16-byte vectors; each thread's
   // units (two at most) are kept in registers from the sums of squares to
-  // the scaling, which runs once the counts are done
+  // the scaling, which runs once the counts are done.  The units go to the
+  // threads of waves 0..6 only: the finishing wave, which publishes the
+  // masks, has no scaling to do after its stores (the compiler would wait
+  // for those stores first)
   const float4* hg = reinterpret_cast<const float4*>(a.h);
   const float4* wg4 = reinterpret_cast<const float4*>(a.norm_w);
-  constexpr int J = (BM * XS + kOT - 1) / kOT;  // units per thread (incl. padding)
+  constexpr int kXT = kOT - kWave;  // threads holding units of h
+  static_assert(kFin == kOW - 1, "the finishing wave is the last one");
+  constexpr int J = (BM * XS + kXT - 1) / kXT;  // units per thread (incl. padding)
   constexpr bool kKeep = J <= 2;
   float4 hr[kKeep ? J : 1][2], wr[kKeep ? J : 1][2];
   // decoder-block mode: x = the fp16 rounding of h * r_t * norm_w, r_t the
   // token's RMS normaliser from the block's sums of squares
   auto scale_x = [&]() {
+    if (tid >= kXT) return;
     float r[BM];
 #pragma unroll
     for (int t = 0; t < BM; ++t) {
@@ -406,7 +412,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-      const int i = tid + j * kOT, t = i / XS, u = i - t * XS;
+      const int i = tid + j * kXT, t = i / XS, u = i - t * XS;
       if (i < BM * XS) {
         u32x4 xv{0, 0, 0, 0};
         if (t < b && u < U) {
@@ -459,8 +465,8 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     for (int t = 0; t < BM; ++t) ss[t] = 0.f;
 #pragma unroll
     for (int j = 0; j < J; ++j) {
-      const int i = tid + j * kOT, t = i / XS, u = i - t * XS;
-      if (i < BM * XS && t < b && u < U) {
+      const int i = tid + j * kXT, t = i / XS, u = i - t * XS;
+      if (tid < kXT && i < BM * XS && t < b && u < U) {
         const float4 p = hg[2 * (t * U + u)], q = hg[2 * (t * U + u) + 1];
         if constexpr (kKeep) {
           hr[j][0] = p;
