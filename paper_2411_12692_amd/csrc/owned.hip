@@ -383,6 +383,20 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       for (int c = lane; c < half_cols; c += kWave) st_agent64(yt + c, 0ull);
     }
   }
+  // decoder-block mode with one token: the tile wave requests its 8 values
+  // of the residual h in the owner's tile now and stores them into y after
+  // the group exchange, so that neither the loads nor the stores delay the
+  // published masks (with more tokens the tile is copied before the first
+  // barrier)
+  float4 htile[2] = {};
+  const int tunit = blk * kWave + lane;  // the lane's unit (8 columns) of the tile
+  if constexpr (block_mode && BM == 1) {
+    if (owns_tile && wv == kTileWave && tunit < U) {
+      const float4* hv4 = reinterpret_cast<const float4*>(a.h);
+      htile[0] = hv4[2 * tunit];
+      htile[1] = hv4[2 * tunit + 1];
+    }
+  }
   // token t's unit u at xs[t * XS + u] (XS = NU * 64 >= U)
   constexpr int XS = OwnedLds<BM, NU>::kUnits;
   // decoder-block mode: h and norm_w as 16-byte vectors; each thread's
@@ -599,12 +613,9 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
     if (predict && any_rows && s + 1 < nsub) __syncthreads();  // the partial counts are reused
   }
-  // decoder-block mode: x itself (for the gate/up products, needed only
-  // after the group exchange) is scaled and rounded now from the registers,
-  // and the owner's tile of y starts as the residual h (while the finishing
-  // wave publishes)
-  if constexpr (block_mode) {
-    if constexpr (kKeep) scale_x();
+  // decoder-block mode with several tokens: the owner's tile of y starts as
+  // the residual h (while the finishing wave publishes)
+  if constexpr (block_mode && BM > 1) {
     if (owns_tile && wv == kTileWave) {
       const int half_cols = min(kTile, d - blk * kTile) / 2;
       for (int t = 0; t < b; ++t) {
@@ -617,6 +628,9 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   __syncthreads();
   n_own = uniform(L.n_own);
   SI_TRACE_MARK(3);
+  // decoder-block mode: x itself, needed only at gate/up, is scaled and
+  // rounded from the registers while the group exchange is under way
+  if constexpr (block_mode && kKeep) scale_x();
 
   bool census_done = false;
   if (a.mlp) {
@@ -654,6 +668,15 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
     census_done = true;
     if (owns_tile && wv == kTileWave) {  // the tile's first stores have landed by now
+      if constexpr (block_mode && BM == 1) {
+        if (tunit < U) {
+          uint64_t* yu = reinterpret_cast<uint64_t*>(a.y) + 4 * (size_t)tunit;
+          st_agent64(yu, ((uint64_t)__float_as_uint(htile[0].y) << 32) | __float_as_uint(htile[0].x));
+          st_agent64(yu + 1, ((uint64_t)__float_as_uint(htile[0].w) << 32) | __float_as_uint(htile[0].z));
+          st_agent64(yu + 2, ((uint64_t)__float_as_uint(htile[1].y) << 32) | __float_as_uint(htile[1].x));
+          st_agent64(yu + 3, ((uint64_t)__float_as_uint(htile[1].w) << 32) | __float_as_uint(htile[1].z));
+        }
+      }
       wait_own_stores();
       if (lane == 0) st_agent64(&a.zflag[blk], tagged(tag, 1u));
     }
