@@ -40,8 +40,9 @@
 // down-projection scales each column of y once, at the tile's add.
 //
 // No block waits for the whole grid: the only exchanges are inside a group.
-// Block 0 adds the published kept counts (the count of the call) and, having
-// seen a word of this call from every block, advances the call counter.
+// One block (the last, where the grid has a block without rows, else block 0)
+// adds the published kept counts (the count of the call) and, having seen a
+// word of this call from every block, advances the call counter.
 // When the caller asks for the ascending kept list, each block adds the
 // counts of the blocks before it at the end and writes its rows' entries.
 //
@@ -336,6 +337,10 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   const int P = gridDim.x, blk = blockIdx.x;
   const int T = a.tiles, R = a.R, nsub = a.nsub;
   const int r0 = blk * R;
+  // the block that takes the census of the blocks' kept counts: one without
+  // rows where the grid has one (the census waits for the last block to
+  // publish, which a block with rows would wait for before its gate/up)
+  const int cblk = a.groups * T < P ? P - 1 : 0;
   const int Rb = blk < a.groups * T ? max(0, min(R, k - r0)) : 0;  // rows this block owns
   const bool predict = a.mask_in == nullptr;
   const bool no_as = (a.flags & kNoAS) != 0;
@@ -645,9 +650,9 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     // the group's mask words, one per thread (waves 0..3), before any
     // gate/up request is out (a round trip behind the grid's row requests
     // would take several times as long)
-    // block 0's waves 4..7 meanwhile take the census: every block's kept
-    // count (the call's count, and proof that every block has read the call
-    // counter, which block 0 then advances)
+    // the census block's waves 4..7 meanwhile take the census: every block's
+    // kept count (the call's count, and proof that every block has read the
+    // call counter, which the census block then advances)
     if (tid < 4 * npairs) {
       const int p = tid >> 2;
       const int o = g * T + p / nsub, sb = p - (p / nsub) * nsub;
@@ -655,12 +660,12 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       uint32_t v[1];
       poll_words<1>(src, 1, tag, a.hdr, v);
       L.pm[tid] = v[0];
-    } else if (blk == 0 && tid >= kOT / 2) {
+    } else if (blk == cblk && tid >= kOT / 2) {
       const int sum = wave_sum_int(census_part(a.pub, P, tid - kOT / 2, kOT / 2, tag, a.hdr));
       if (lane == 0) L.wsum[wv] = sum;
     }
     __syncthreads();
-    if (blk == 0 && tid == 0) {
+    if (blk == cblk && tid == 0) {
       int sum = 0;
       for (int w = kOW / 2; w < kOW; ++w) sum += L.wsum[w];
       if (a.n_out) *a.n_out = sum;
@@ -928,7 +933,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       a.counts[2 * blk + 1] = L.n_down;
     }
   }
-  if (blk == 0 && !census_done) {  // the predictor alone: the census of block 0
+  if (blk == cblk && !census_done) {  // the predictor alone: the census at the end
     const int sum = block_sum(L, census_part(a.pub, P, tid, kOT, tag, a.hdr), lane, wv);
     if (tid == 0) {
       if (a.n_out) *a.n_out = sum;
