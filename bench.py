@@ -67,6 +67,7 @@ def algorithmic_bytes(k, d, b, n_gate, n_up, n_down, block=False, int8=False):
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_7b_s0.9_counters.txt")
 RELU_COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_opt6.7b_relu_s0.9_counters.txt")
 INT8_COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_7b_int8_s0.9_counters.txt")
+BLOCK_COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_7b_block_s0.9_counters.txt")
 KERNEL_SOURCES = ("paper_2411_12692_amd/csrc/owned.hip", "paper_2411_12692_amd/csrc/layer_common.h",
                   "paper_2411_12692_amd/csrc/si_device.h")
 
@@ -665,8 +666,8 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None if block else measured_traffic(RELU_COUNTERS_FILE if relu else
-                                                           INT8_COUNTERS_FILE if int8 else COUNTERS_FILE),
+            "traffic": measured_traffic(RELU_COUNTERS_FILE if relu else INT8_COUNTERS_FILE if int8 else
+                                        BLOCK_COUNTERS_FILE if block else COUNTERS_FILE),
             "launch_us": round(us_per_layer, 3),
             "isolated_launch_us": round(isolated_us, 3),
         },
