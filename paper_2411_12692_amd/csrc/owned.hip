@@ -824,58 +824,117 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     const bool dcol_ok = dunit < U;
     constexpr bool kZLane = kODN * BM < kWave;  // wave 0's lane 63 is free for the zero flag
     typedef DownPiece<kI8> DP;
-    for (int q0 = 0; q0 < dN; q0 += kODownRound) {
-      typename DP::type vd[kODN];
-      uint32_t dl = 0;
+    // with 2..8 tokens the rounds are pipelined: once round r's h3 words are
+    // in (which also waits for its pieces), round r+1's pieces are requested
+    // and round r's products (8 tokens x 8 columns per piece, the down
+    // projection's arithmetic) run while they are in flight.  Every kept
+    // row's pieces are requested (with several tokens a kept row almost
+    // always has a non-zero h3; without speculation the rounds below run)
+    bool pipelined = false;
+    if constexpr (BM >= 2) {
+      if (spec_ok && dN > 0) {
+        pipelined = true;
+        const int dcu = min(dunit, U - 1);  // column unit of the loads (in the row even past d)
+        typename DP::type va[kODN], vb[kODN];
+        auto request = [&](int q0, typename DP::type(&v)[kODN]) {
 #pragma unroll
-      for (int j = 0; j < kODN; ++j) {
-        vd[j] = typename DP::type{};
-        const int q = q0 + wv + kOW * j;
-        if (q < dN) {
-          const uint32_t e = L.dent[q];
-          if ((spec_ok && (e >> 31)) || no_as) {
+          for (int j = 0; j < kODN; ++j) {
+            const int q = min(q0 + wv + kOW * j, dN - 1);
+            v[j] = DP::load(a.wdt, L.dent[q] & 0x7fffffffu, U, dcu);
+          }
+        };
+        auto round = [&](int q0, typename DP::type(&cur)[kODN], typename DP::type(&nxt)[kODN]) {
+          const int pj = lane / BM, pt = lane - pj * BM;
+          const int pq = q0 + wv + kOW * pj;
+          const bool pok = pj < kODN && pq < dN && pt < b;
+          const bool zlane = kZLane && q0 == 0 && wv == 0 && lane == kWave - 1;
+          const uint64_t* src[1] = {zlane ? &a.zflag[tile]
+                                          : a.h3e + (size_t)(L.dent[pok ? pq : q0] & 0x7fffffffu) * b + (pok ? pt : 0)};
+          uint32_t hw[1];
+          poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
+          if (q0 == 0 && wv == 0) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
+          if (q0 == 0) SI_TRACE_WAVE(3);
+          if (q0 + kODownRound < dN) request(q0 + kODownRound, nxt);
+#pragma unroll
+          for (int j = 0; j < kODN; ++j) {
+            const int q = q0 + wv + kOW * j;
+            float hv[BM];
+#pragma unroll
+            for (int t = 0; t < BM; ++t)
+              hv[t] = (j * BM + t < kWave && q < dN && t < b)
+                          ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(hw[0], min(j * BM + t, kWave - 1)))
+                          : 0.f;
+            n_down += q < dN ? 1 : 0;
+            float f[8];
+            DP::values(cur[j], f);
+#pragma unroll
+            for (int t = 0; t < BM; ++t)
+#pragma unroll
+              for (int qq = 0; qq < 8; ++qq) acc[t][qq] = fmaf(hv[t], f[qq], acc[t][qq]);
+          }
+          if (q0 == 0) SI_TRACE_WAVE(4);
+        };
+        request(0, va);
+        for (int q0 = 0; q0 < dN; q0 += 2 * kODownRound) {
+          round(q0, va, vb);
+          if (q0 + kODownRound < dN) round(q0 + kODownRound, vb, va);
+        }
+      }
+    }
+    if (!pipelined) {
+      for (int q0 = 0; q0 < dN; q0 += kODownRound) {
+        typename DP::type vd[kODN];
+        uint32_t dl = 0;
+#pragma unroll
+        for (int j = 0; j < kODN; ++j) {
+          vd[j] = typename DP::type{};
+          const int q = q0 + wv + kOW * j;
+          if (q < dN) {
+            const uint32_t e = L.dent[q];
+            if ((spec_ok && (e >> 31)) || no_as) {
+              if (dcol_ok) vd[j] = DP::load(a.wdt, e & 0x7fffffffu, U, dunit);
+              dl |= 1u << j;
+            }
+          }
+        }
+        // h3 of (piece j, token t) in lane j * BM + t
+        const int pj = lane / BM, pt = lane - pj * BM;
+        const int pq = q0 + wv + kOW * pj;
+        const bool pok = pj < kODN && pq < dN && pt < b;
+        const bool zlane = kZLane && q0 == 0 && wv == 0 && lane == kWave - 1;
+        const uint64_t* src[1] = {zlane ? &a.zflag[tile]
+                                        : a.h3e + (size_t)(L.dent[pok ? pq : q0] & 0x7fffffffu) * b + (pok ? pt : 0)};
+        uint32_t hw[1];
+        poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
+        if (q0 == 0 && wv == 0) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
+        if (q0 == 0) SI_TRACE_WAVE(3);
+#pragma unroll
+        for (int j = 0; j < kODN; ++j) {
+          const int q = q0 + wv + kOW * j;
+          float hv[BM];
+          bool nz = false;
+#pragma unroll
+          for (int t = 0; t < BM; ++t) {
+            hv[t] = (j * BM + t < kWave && q < dN && t < b)
+                        ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(hw[0], min(j * BM + t, kWave - 1)))
+                        : 0.f;
+            nz |= hv[t] != 0.f;
+          }
+          if (q < dN && !((dl >> j) & 1u) && nz) {  // late request
+            const uint32_t e = L.dent[q];
             if (dcol_ok) vd[j] = DP::load(a.wdt, e & 0x7fffffffu, U, dunit);
             dl |= 1u << j;
           }
+          float f[8];
+          DP::values(vd[j], f);
+#pragma unroll
+          for (int t = 0; t < BM; ++t)
+#pragma unroll
+            for (int qq = 0; qq < 8; ++qq) acc[t][qq] = fmaf(hv[t], f[qq], acc[t][qq]);
         }
+        n_down += __popc(dl);
+        if (q0 == 0) SI_TRACE_WAVE(4);
       }
-      // h3 of (piece j, token t) in lane j * BM + t
-      const int pj = lane / BM, pt = lane - pj * BM;
-      const int pq = q0 + wv + kOW * pj;
-      const bool pok = pj < kODN && pq < dN && pt < b;
-      const bool zlane = kZLane && q0 == 0 && wv == 0 && lane == kWave - 1;
-      const uint64_t* src[1] = {zlane ? &a.zflag[tile]
-                                      : a.h3e + (size_t)(L.dent[pok ? pq : q0] & 0x7fffffffu) * b + (pok ? pt : 0)};
-      uint32_t hw[1];
-      poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
-      if (q0 == 0 && wv == 0) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
-      if (q0 == 0) SI_TRACE_WAVE(3);
-#pragma unroll
-      for (int j = 0; j < kODN; ++j) {
-        const int q = q0 + wv + kOW * j;
-        float hv[BM];
-        bool nz = false;
-#pragma unroll
-        for (int t = 0; t < BM; ++t) {
-          hv[t] = (j * BM + t < kWave && q < dN && t < b)
-                      ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(hw[0], min(j * BM + t, kWave - 1)))
-                      : 0.f;
-          nz |= hv[t] != 0.f;
-        }
-        if (q < dN && !((dl >> j) & 1u) && nz) {  // late request
-          const uint32_t e = L.dent[q];
-          if (dcol_ok) vd[j] = DP::load(a.wdt, e & 0x7fffffffu, U, dunit);
-          dl |= 1u << j;
-        }
-        float f[8];
-        DP::values(vd[j], f);
-#pragma unroll
-        for (int t = 0; t < BM; ++t)
-#pragma unroll
-          for (int qq = 0; qq < 8; ++qq) acc[t][qq] = fmaf(hv[t], f[qq], acc[t][qq]);
-      }
-      n_down += __popc(dl);
-      if (q0 == 0) SI_TRACE_WAVE(4);
     }
     if (lane == 0 && tile == 0 && n_down) atomicAdd(&L.n_down, n_down);
     if (wv == 0 && lane == 0) L.wsum[0] = zok ? 1 : 0;
