@@ -12,6 +12,12 @@ namespace {
 
 thread_local char g_err[512] = "";
 
+// Rows with N_neg < T - margin count as surely kept: their W_up and W_down^T
+// requests go out before the gate result.  With 5-8 tokens the union of the
+// tokens' kept sets covers nearly every row, so every kept row is treated so
+// (margin 0): the few wasted W_up reads cost less than waiting for the gate.
+int confident_margin(int d, int b) { return b > 4 ? 0 : d / 16; }
+
 si_status fail(si_status s, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
@@ -271,7 +277,7 @@ si_status predict_sparse_mlp_impl(const uint32_t* signs, const uint16_t* w_gate,
     c.d = d;
     c.b = b;
     c.T = T;
-    c.margin = d / 16;  // rows with N_neg < T - d/16 are treated as surely kept (speculative W_up / W_down^T requests)
+    c.margin = confident_margin(d, b);
     c.flags = flags;
     c.mask = mask;
     c.idx = active_idx;
@@ -373,7 +379,7 @@ si_status si_rmsnorm_predict_sparse_mlp(const float* h, const float* norm_w, flo
   c.d = d;
   c.b = b;
   c.T = si_alpha_threshold(alpha, d);
-  c.margin = d / 16;
+  c.margin = confident_margin(d, b);
   c.flags = flags;
   c.mask = mask;
   c.idx = active_idx;
@@ -450,7 +456,7 @@ si_status int8_impl(bool predict, const uint32_t* signs, const int8_t* w_gate, c
   c.b = b;
   if (predict) {
     c.T = si_alpha_threshold(alpha, d);
-    c.margin = d / 16;
+    c.margin = confident_margin(d, b);
     c.mask = mask;
     c.idx = active_idx;
   }
