@@ -277,6 +277,22 @@ def test_batch_union(b):
         check_mlp(c, c.x, m_ref, y, cnt)
 
 
+@pytest.mark.parametrize("b", [4, 5, 8])
+def test_batch_7b_fused(b):
+    """The fused call at the 7B shape with 4 to 8 tokens.  With 5 or more,
+    every kept row's W_up and W_down^T rows are requested before its gate
+    result: rows whose ReLU output turns out zero must add nothing to y, and
+    the read counters may exceed the oracle's n_up and n_down but never
+    n_gate."""
+    c = Case.planted(4096, 11008, 0.9, config=2, b=b)
+    y, (mask, idx, n, cnt) = c.layer(to_dev(c.x), 1.0, outputs=True)
+    torch.cuda.synchronize()
+    m_ref = check_predict(c, c.x, 1.0)
+    assert np.array_equal(mask.cpu().numpy(), m_ref)
+    check_list(idx, n, m_ref)
+    check_mlp(c, c.x, m_ref, y, cnt)
+
+
 @pytest.mark.parametrize("k,d,b", [(700, 8192, 5), (700, 8192, 8), (1500, 5120, 8), (1300, 4096, 7)])
 def test_batch_wide_rows(k, d, b):
     """Batches of 5 to 8 tokens with the widest rows: the token block fills
