@@ -16,12 +16,13 @@ Steps cycle through a pool of independently seeded layers whose weights
 from HBM.  The timed loop is replayed from a HIP graph (the per-call host
 cost of Python would otherwise dominate a ~10 us step).
 
-``--report alpha|stacks|sweep`` prints the other measurements of the
+``--report alpha|stacks|sweep|paths`` prints the other measurements of the
 workloads instead, one JSON line per point: the alpha sweep of the 7B layer
 (time, bytes, recall, speedup over the dense call), the 32-layer 7B and
 40-layer 13B decode stacks (us per layer and tokens/s, chained through the
-stacks' glue, plus the predictor alone), and the sparsity x batch sweep
-(sparse against dense calls at the same batch, and where dense wins).
+stacks' glue, plus the predictor alone), the sparsity x batch sweep
+(sparse against dense calls at the same batch, and where dense wins), and
+the 7B layer through each call form (mask, list, predictor, fused, dense).
 
 Prints one JSON line.  ``value`` is the effective HBM bandwidth on the
 algorithmic bytes of a step (packed signs + x + the kept rows of W_gate,
@@ -113,9 +114,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--launches", type=int, default=256, help="individually timed launches for the roofline")
-    ap.add_argument("--report", choices=("alpha", "stacks", "sweep"), default=None,
+    ap.add_argument("--report", choices=("alpha", "stacks", "sweep", "paths"), default=None,
                     help="alpha: the alpha sweep of the 7B layer; stacks: the 7B and 13B decode stacks; sweep: "
-                         "sparsity x batch against dense (JSON line per point; no headline line)")
+                         "sparsity x batch against dense; paths: each call form at 1-8 tokens (JSON line per point; no headline line)")
     ap.add_argument("--tokens", type=int, default=256, help="decode steps of --report stacks")
     ap.add_argument("--profile-pass", action="store_true",
                     help="for hardware-counter runs: eager layer calls over the pool, then one plain 256 MiB "
@@ -520,6 +521,51 @@ def report_sweep(args, si, synth, dev):
         torch.cuda.empty_cache()
 
 
+def report_paths(args, si, synth, dev):
+    """The 7B shape through each call form, us per call (graph replay over a
+    pool of 8 layers), at planted s = 0.9 and 0.5 and 1, 2, 4, 8 tokens: the
+    sparse MLP from the batch's union mask (the per-token planted sets, as
+    in the sweep) and from the same rows as a list, the predictor alone, the
+    fused predict + MLP (which keeps the rows its own prediction gives), and
+    the dense call (every row kept)."""
+    import torch
+
+    L = 8
+    for s_ in (0.9, 0.5):
+        pls = [synth.planted_layer(D, K, s_, config=5, layer=l, device=dev) for l in range(L)]
+        layers = [si.MLPLayer(p.w_gate, p.w_up, p.w_down, max_batch=8) for p in pls]
+        ones = torch.ones(K, dtype=torch.uint8, device=dev)
+        for b in (1, 2, 4, 8):
+            xs = [synth.batch_tokens(p, b, config=5, layer_id=l) for l, p in enumerate(pls)]
+            ms = [synth.batch_union_mask(p, b, config=5, layer_id=l) for l, p in enumerate(pls)]
+            lists = []
+            for m in ms:
+                nz = torch.nonzero(m).flatten().to(torch.int32)
+                idx = torch.zeros(K, dtype=torch.int32, device=dev)
+                idx[: nz.numel()] = nz
+                lists.append((idx, torch.tensor([nz.numel()], dtype=torch.int32, device=dev)))
+            ys = [torch.empty(b, D, dtype=torch.float32, device=dev) for _ in range(L)]
+            fused_rows = 0
+            for l in range(L):
+                _, (_, _, n, _) = layers[l](xs[l], 1.0, outputs=True)
+                fused_rows += int(n.item())
+            row = {
+                "report": "paths", "s": s_, "b": b,
+                "union_rows_mean": sum(int(m.sum()) for m in ms) / L,
+                "fused_rows_mean": fused_rows / L,
+                "mask_us": graph_us(lambda i: layers[i % L].sparse_mlp(xs[i % L], mask=ms[i % L]), 4 * L, reps=8),
+                "list_us": graph_us(lambda i: layers[i % L].sparse_mlp(xs[i % L], ms[i % L], *lists[i % L]),
+                                    4 * L, reps=8),
+                "predict_us": graph_us(lambda i: layers[i % L].predict(xs[i % L], 1.0), 4 * L, reps=8),
+                "fused_us": graph_us(lambda i: layers[i % L](xs[i % L], 1.0, y=ys[i % L]), 4 * L, reps=8),
+                "dense_us": graph_us(lambda i: layers[i % L].sparse_mlp(xs[i % L], mask=ones), 4 * L, reps=8),
+                "workload": f"7B-shaped layer d={D} k={K}, planted s={s_}, {b} tokens, pool of {L}",
+            }
+            print(json.dumps({k: round(v, 3) if isinstance(v, float) else v for k, v in row.items()}), flush=True)
+        del layers, pls
+        torch.cuda.empty_cache()
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -542,7 +588,7 @@ def main():
     torch.cuda.set_device(dev)
     si._lib.load()  # fails loudly if the library is not built
     if args.report:
-        {"alpha": report_alpha, "stacks": report_stacks, "sweep": report_sweep}[args.report](args, si, synth, dev)
+        {"alpha": report_alpha, "stacks": report_stacks, "sweep": report_sweep, "paths": report_paths}[args.report](args, si, synth, dev)
         return
 
     relu = args.mlp == "relu"

@@ -202,6 +202,17 @@ si_status sparse_mlp_impl(const uint16_t* w_gate, const uint16_t* w_up, const ui
   hipStream_t st = (hipStream_t)stream;
   const si::WsLayout L = si::ws_layout(k, b);
   char* base = static_cast<char*>(workspace);
+  if (active_idx && b > 4 && si::owned_supported(k, d, b)) {
+    // With 5-8 tokens the list-driven kernel (16 waves per block, so at most
+    // 128 registers per lane) spills; the list becomes a mask in the
+    // workspace and the row-owning kernel (8 waves) runs in mask mode.
+    uint8_t* wmask = reinterpret_cast<uint8_t*>(base + L.mask);
+    if (si_status s = hip_status(si::launch_list_to_mask(active_idx, n_active, k, wmask, st), "list launch"))
+      return s;
+    mask = wmask;
+    active_idx = nullptr;
+    n_active = nullptr;
+  }
   if (active_idx ? si::layer_supported(k, d, b) : si::owned_supported(k, d, b)) {
     si::LayerCall c;
     c.w_gate = w_gate;

@@ -261,6 +261,27 @@ __global__ __launch_bounds__(1024) void k_compact(const uint8_t* __restrict__ ma
   if (tid == 0) *n_out = base;
 }
 
+// ascending list of n rows (n read from n_in) -> [k] mask (1 = listed): the
+// block clears every byte, then sets the listed rows; entries outside
+// [0, k) are ignored.
+__global__ __launch_bounds__(1024) void k_list_to_mask(const int32_t* __restrict__ idx,
+                                                       const int32_t* __restrict__ n_in, int k,
+                                                       uint8_t* __restrict__ mask) {
+  const int tid = threadIdx.x;
+  for (int i = tid; i < k; i += 1024) mask[i] = 0;
+  const int n = min(max(*n_in, 0), k);
+  __syncthreads();
+  for (int j = tid; j < n; j += 1024) {
+    const int r = idx[j];
+    if (r >= 0 && r < k) mask[r] = 1;
+  }
+}
+
+hipError_t launch_list_to_mask(const int32_t* idx, const int32_t* n_in, int k, uint8_t* mask, hipStream_t s) {
+  k_list_to_mask<<<1, 1024, 0, s>>>(idx, n_in, k, mask);
+  return hipGetLastError();
+}
+
 hipError_t launch_compact(const uint8_t* mask, int k, int32_t* idx, int32_t* n_out, hipStream_t s) {
   k_compact<<<1, 1024, 0, s>>>(mask, k, idx, n_out);
   return hipGetLastError();

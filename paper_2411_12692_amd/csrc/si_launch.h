@@ -77,6 +77,9 @@ hipError_t launch_owned(const LayerCall& c, hipStream_t s);
 // mask -> ascending kept list and count (single block).
 hipError_t launch_compact(const uint8_t* mask, int k, int32_t* idx, int32_t* n_out, hipStream_t s);
 
+// ascending kept list and count -> [k] mask (single block).
+hipError_t launch_list_to_mask(const int32_t* idx, const int32_t* n_in, int k, uint8_t* mask, hipStream_t s);
+
 // Sparse gate/up (+ReLU, product, actual sparsity) and sparse down.
 hipError_t launch_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint16_t* w_down_t,
                              int k, int d, const uint16_t* x, int b, const int32_t* idx,

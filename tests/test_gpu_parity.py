@@ -293,6 +293,30 @@ def test_batch_7b_fused(b):
     check_mlp(c, c.x, m_ref, y, cnt)
 
 
+@pytest.mark.parametrize("b", [5, 8])
+def test_list_form_batch_7b(b):
+    """The list form with 5 to 8 tokens at the 7B shape (there the list is
+    turned into a mask in the workspace for the row-owning kernel): a call
+    with every row listed, then one with the predicted rows and garbage past
+    n, must each give the oracle's result on its own rows."""
+    c = Case.planted(4096, 11008, 0.9, config=2, b=b)
+    x = to_dev(c.x)
+    m_ref = oracle.predict_rows(c.packed, c.x, 1.0)[0]
+    all_idx = torch.arange(c.k, dtype=torch.int32, device=DEV)
+    all_n = torch.tensor([c.k], dtype=torch.int32, device=DEV)
+    y0, c0 = c.layer.sparse_mlp(x, None, all_idx, all_n, counters=True)
+    torch.cuda.synchronize()
+    check_mlp(c, c.x, np.ones(c.k, dtype=bool), y0, c0)
+    rows = np.flatnonzero(m_ref)
+    idx = np.full(c.k, c.k + 5, dtype=np.int32)
+    idx[rows.size:] = np.where(np.arange(c.k - rows.size) % 2 == 0, -7, c.k + 5)
+    idx[: rows.size] = rows
+    y1, c1 = c.layer.sparse_mlp(x, None, torch.from_numpy(idx).to(DEV),
+                                torch.tensor([rows.size], dtype=torch.int32, device=DEV), counters=True)
+    torch.cuda.synchronize()
+    check_mlp(c, c.x, m_ref, y1, c1)
+
+
 @pytest.mark.parametrize("k,d,b", [(700, 8192, 5), (700, 8192, 8), (1500, 5120, 8), (1300, 4096, 7)])
 def test_batch_wide_rows(k, d, b):
     """Batches of 5 to 8 tokens with the widest rows: the token block fills
