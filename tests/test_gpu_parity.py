@@ -339,6 +339,41 @@ def test_batch_wide_rows(k, d, b):
         check_mlp(c, c.x, m_ref, y2, c2)
 
 
+@pytest.mark.parametrize("seed", range(12))
+def test_random_shapes_every_form(seed):
+    """Seeded random shapes (d a multiple of 128 up to 8192, k up to 20000,
+    1 to 8 tokens, alpha from 0.7 to +inf): the fused call against the
+    oracle's prediction and MLP, then a random mask of random density through
+    the mask form and the same rows through the list form."""
+    rng = np.random.default_rng(4100 + seed)
+    d = 128 * int(rng.integers(1, 65))
+    k = int(rng.integers(1, min(20000, 6_000_000 // d) + 1))
+    b = int(rng.integers(1, 9))
+    alpha = float(rng.choice([0.7, 1.0, 1.03, 1.45, math.inf]))
+    print(f"seed={seed} k={k} d={d} b={b} alpha={alpha}", flush=True)
+    c = Case(rand_bits(rng, (k, d), False), rand_bits(rng, (k, d), False), rand_bits(rng, (d, k), False),
+             rand_bits(rng, (b, d), seed % 2 == 0), max_batch=b)
+    x = to_dev(c.x)
+    y, (mask, idx, n, cnt) = c.layer(x, alpha, outputs=True)
+    torch.cuda.synchronize()
+    m_ref = oracle.predict_rows(c.packed, c.x, alpha)[0]
+    assert np.array_equal(mask.cpu().numpy(), m_ref)
+    check_list(idx, n, m_ref)
+    if m_ref.any():
+        check_mlp(c, c.x, m_ref, y, cnt)
+    m = rng.random(k) < rng.uniform(0.02, 1.0)
+    m[int(rng.integers(0, k))] = True
+    rows = np.flatnonzero(m).astype(np.int32)
+    y1, c1 = c.layer.sparse_mlp(x, mask=torch.from_numpy(m.astype(np.uint8)).to(DEV), counters=True)
+    lst = np.full(k, -1, dtype=np.int32)
+    lst[: rows.size] = rows
+    y2, c2 = c.layer.sparse_mlp(x, None, torch.from_numpy(lst).to(DEV),
+                                torch.tensor([rows.size], dtype=torch.int32, device=DEV), counters=True)
+    torch.cuda.synchronize()
+    check_mlp(c, c.x, m, y1, c1)
+    check_mlp(c, c.x, m, y2, c2)
+
+
 @pytest.mark.parametrize("k,d", [(1, 128), (63, 128), (65, 384), (129, 8192), (1000, 640), (1, 8192),
                                  (20000, 384), (65536, 128)])
 def test_sparse_mlp_edge_shapes(k, d):
