@@ -217,6 +217,30 @@ def test_int8_edge_shapes(k, d, b):
             check(c, m_ref, y, cnt)
 
 
+@pytest.mark.parametrize("seed", range(8))
+def test_int8_random_shapes(seed):
+    """Seeded random shapes (d a multiple of 128 up to 8192, k up to 12000,
+    1 to 8 tokens, gated or not, alpha from 0.7 to +inf): the device's INT8
+    weights and the fused call against the oracle, then a random mask of
+    random density through the mask form."""
+    rng = np.random.default_rng(5200 + seed)
+    d = 128 * int(rng.integers(1, 65))
+    k = int(rng.integers(1, min(12000, 4_000_000 // d) + 1))
+    b = int(rng.integers(1, 9))
+    gated = seed % 3 != 2
+    alpha = float(rng.choice([0.7, 1.0, 1.03, 1.45, math.inf]))
+    print(f"seed={seed} k={k} d={d} b={b} gated={gated} alpha={alpha}", flush=True)
+    c = I8Case(rand_bits(rng, (k, d)), rand_bits(rng, (k, d)) if gated else None, rand_bits(rng, (d, k)),
+               rand_bits(rng, (b, d)), max_batch=b)
+    check_weights(c)
+    fused(c, alpha)
+    m = rng.random(k) < rng.uniform(0.02, 1.0)
+    m[int(rng.integers(0, k))] = True
+    y, cnt = c.layer.sparse_mlp(to_dev(c.x), torch.from_numpy(m.astype(np.uint8)).to(DEV), counters=True)
+    torch.cuda.synchronize()
+    check(c, m, y, cnt)
+
+
 def test_int8_rejects_bad_arguments(tiny):
     lib = si._lib.load()
     L = tiny.layer
