@@ -148,3 +148,22 @@ def test_block_rejects_bad_arguments():
     assert call(None, y, 1e-5) == si._lib.SI_ERR_NULL
     assert call(h, y, 1e-5) == 0
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_block_random_shapes(seed):
+    """Seeded random shapes of the decoder-block call (d a multiple of 128
+    up to 8192, k up to 12000, 1 to 8 tokens, gated or not, alpha from 0.7 to
+    +inf), with h of random scale and a norm weight of either sign."""
+    rng = np.random.default_rng(6300 + seed)
+    d = 128 * int(rng.integers(1, 65))
+    k = int(rng.integers(1, min(12000, 4_000_000 // d) + 1))
+    b = int(rng.integers(1, 9))
+    gated = seed % 3 != 1
+    alpha = float(rng.choice([0.7, 1.0, 1.03, 1.45, math.inf]))
+    print(f"seed={seed} k={k} d={d} b={b} gated={gated} alpha={alpha}", flush=True)
+    h = (rng.standard_normal((b, d)) * rng.uniform(0.1, 10.0)).astype(np.float32)
+    nw = (rng.uniform(0.2, 2.0, d) * np.where(rng.random(d) < 0.1, -1.0, 1.0)).astype(np.float32)
+    c = BlockCase(rand_bits(rng, (k, d)), rand_bits(rng, (k, d)) if gated else None, rand_bits(rng, (d, k)), h, nw,
+                  1e-5, max_batch=b)
+    c.check(alpha)
