@@ -459,19 +459,41 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       }
     }
   };
-  if constexpr (!block_mode) {
+  if constexpr (!block_mode && BM == 1) {
     const u32x4* xg = reinterpret_cast<const u32x4*>(a.x);
-    const int nx = b * U;
-    for (int i = tid; i < BM * XS; i += kOT) {
-      const int t = i / XS, u = i - t * XS;
-      const u32x4 xv = xg[min(t * U + u, nx - 1)];
+    for (int i = tid; i < XS; i += kOT) {
+      const u32x4 xv = xg[min(i, U - 1)];
       if (i == tid && tid == 0) {
         asm volatile("" ::: "memory");
         L.epoch = ld_agent(&a.hdr[H_EPOCH]);
         L.n_up = 0;
         L.n_down = 0;
       }
-      L.xs[i] = (t < b && u < U) ? xv : u32x4{0, 0, 0, 0};
+      L.xs[i] = i < U ? xv : u32x4{0, 0, 0, 0};
+    }
+  } else if constexpr (!block_mode) {
+    // with 2-8 tokens every unit of the thread is requested before any is
+    // stored, so that the requests travel together (a load-store loop
+    // waits once per unit: 2 us of 64 KB with 8 tokens)
+    const u32x4* xg = reinterpret_cast<const u32x4*>(a.x);
+    const int nx = b * U;
+    constexpr int JX = (BM * XS + kOT - 1) / kOT;
+    u32x4 xv[JX];
+#pragma unroll
+    for (int j = 0; j < JX; ++j) {
+      const int i = tid + j * kOT, t = i / XS, u = i - t * XS;
+      xv[j] = xg[min(t * U + u, nx - 1)];
+    }
+    if (tid == 0) {
+      asm volatile("" ::: "memory");
+      L.epoch = ld_agent(&a.hdr[H_EPOCH]);
+      L.n_up = 0;
+      L.n_down = 0;
+    }
+#pragma unroll
+    for (int j = 0; j < JX; ++j) {
+      const int i = tid + j * kOT, t = i / XS, u = i - t * XS;
+      if (i < BM * XS) L.xs[i] = (t < b && u < U) ? xv[j] : u32x4{0, 0, 0, 0};
     }
   } else {
     // decoder-block mode: x = RMSNorm(h) * norm_w in fp16, formed here from
