@@ -25,13 +25,18 @@ stacks' glue, plus the predictor alone), the sparsity x batch sweep
 the 7B layer through each call form (mask, list, predictor, fused, dense).
 
 Prints one JSON line.  ``value`` is the effective HBM bandwidth on the
-algorithmic bytes of a step (packed signs + x + the kept rows of W_gate,
-W_up and W_down^T + y), divided by the measured time per step.
+algorithmic bytes of a step (packed signs + x + the kept rows of W_gate and
+the rows of W_up and W_down^T that actual sparsity needs, from the values +
+y), divided by the measured time per step.  Exactly ``--warmup`` untimed
+steps run first, then exactly ``--steps`` timed steps from one graph.
+``measured_peak`` is the streaming-read bandwidth of a plain read kernel
+(``si_read_bandwidth_probe``) in the same run.
 """
 
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
 import math
 import os
@@ -113,6 +118,7 @@ def parse():
                          "7B layer with INT8 weights")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-peak", action="store_true", help="skip the streaming-read probe")
     ap.add_argument("--launches", type=int, default=256, help="individually timed launches for the roofline")
     ap.add_argument("--report", choices=("alpha", "stacks", "sweep", "paths"), default=None,
                     help="alpha: the alpha sweep of the 7B layer; stacks: the 7B and 13B decode stacks; sweep: "
@@ -139,6 +145,18 @@ def profile_pass(step, n_layers, calls, dev):
         dst.copy_(src)
     torch.cuda.synchronize()
     print(f"# profile pass: {calls} layer calls, 4 copies of {src.numel() * 2} bytes", file=sys.stderr, flush=True)
+
+
+def cpu_model():
+    """The host CPU's model name from /proc/cpuinfo (what the oracle ran on)."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 def _oracle_pass(layers_host, alpha, budget_s, k, d, block, int8, threads):
@@ -199,7 +217,7 @@ def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None, int8=False)
         "kind": "oracle",
         "sample": f"{calls} layer calls over the first {len(layers_host)} layers of the pool "
                   f"({what}, numpy float64, 1 thread, {total_s:.1f} s)",
-        "cpu": platform.processor() or platform.machine(),
+        "cpu": cpu_model(),
         "all_cores": {"value": round(mt_bytes / mt_s / 1e9, 3), "unit": "GB/s",
                       "us_per_layer": round(mt_s / mt_calls * 1e6, 1), "threads": mt_threads,
                       "affinity_cores": ncores, "os_cpu_count": os.cpu_count(),
@@ -208,40 +226,103 @@ def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None, int8=False)
     }
 
 
-def time_graph(step, n_layers, steps_wanted, warmup_wanted):
-    """Replay a HIP graph of back-to-back steps (one pass over the layer pool
-    or more) and return (us per step, steps, warm-up steps, wall us per
-    step); events on the replay stream bracket the timed replays."""
+def time_steps(step, steps, warmup):
+    """Exactly ``warmup`` untimed steps (launched one by one on the timing
+    stream), then exactly ``steps`` timed steps replayed from one HIP graph of
+    ``steps`` launches (step i runs layer i mod pool, continuing the
+    rotation).  Events on the replay stream bracket the one replay, with a
+    synchronization on both sides.  Returns (us per step, wall us per step)."""
     import torch
 
     stream = torch.cuda.Stream()
-    per_graph = n_layers * max(1, 64 // n_layers)
     with torch.cuda.stream(stream):
-        for i in range(per_graph):  # warm the path on the capture stream
+        for i in range(warmup):
             step(i)
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=stream):
-        for i in range(per_graph):
+        for i in range(warmup, warmup + steps):
             step(i)
-    torch.cuda.synchronize()
-    reps = max(1, math.ceil(steps_wanted / per_graph))
-    wreps = max(1, math.ceil(warmup_wanted / per_graph))
-    steps, warmup = reps * per_graph, wreps * per_graph
-    for _ in range(wreps):
-        graph.replay()
     torch.cuda.synchronize()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     e0.record(stream)
     with torch.cuda.stream(stream):
-        for _ in range(reps):
-            graph.replay()
+        graph.replay()
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    return e0.elapsed_time(e1) * 1e3 / steps, steps, warmup, wall * 1e6 / steps
+    del graph
+    return e0.elapsed_time(e1) * 1e3 / steps, wall * 1e6 / steps
+
+
+def truth_counts(mask, x, w_gate, w_up):
+    """Rows the method itself must read for one call (its algorithmic work),
+    from the values, not from what the kernel requested: ``n_gate`` = kept
+    rows; ``n_up`` = kept rows where some token's gate value is positive (the
+    W_up rows actual sparsity needs; 0 without W_up); ``n_down`` = kept rows
+    where some token's h3 is non-zero (h1 > 0 and, gated, u != 0).  Gate and
+    up values are fp32 products of the tokens with the weight values on the
+    device (``w_gate`` / ``w_up`` fp16 tensors, or float32 dequantized
+    INT8 values)."""
+    xs = x.reshape(-1, w_gate.shape[1]).float()
+    kept = mask.reshape(-1).bool()
+    pos = ((xs @ w_gate.float().t()) > 0).any(dim=0) & kept
+    if w_up is None:
+        return [int(kept.sum()), 0, int(pos.sum())]
+    g = xs @ w_gate.float().t()
+    u = xs @ w_up.float().t()
+    nz = ((g > 0) & (u != 0)).any(dim=0) & kept
+    return [int(kept.sum()), int(pos.sum()), int(nz.sum())]
+
+
+def measured_read_peak(si, dev, total_bytes=4 << 30, slice_bytes=32 << 20):
+    """Streaming-read bandwidth of the device with the library's plain read
+    kernel (``si_read_bandwidth_probe``): (a) one launch over a 4 GiB buffer
+    (16x the Infinity Cache), best of 3; (b) 32 MiB per launch (the size of a
+    7B layer call) over 128 different slices, replayed from a graph, so that
+    the per-launch cost is included."""
+    import torch
+
+    buf = torch.zeros(total_bytes, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(4, dtype=torch.int32, device=dev)
+    stream = torch.cuda.Stream()
+
+    def probe(off, n):
+        si._lib.call("si_read_bandwidth_probe", ctypes.c_void_p(buf.data_ptr() + off), n,
+                     ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+
+    best = 0.0
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        probe(0, total_bytes)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        best = max(best, total_bytes / (e0.elapsed_time(e1) * 1e-3) / 1e9)
+    n_slices = total_bytes // slice_bytes
+    with torch.cuda.stream(stream):
+        probe(0, slice_bytes)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for i in range(n_slices):
+            probe(i * slice_bytes, slice_bytes)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    with torch.cuda.stream(stream):
+        for _ in range(4):
+            g.replay()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us_slice = e0.elapsed_time(e1) * 1e3 / (4 * n_slices)
+    del g, buf
+    torch.cuda.empty_cache()
+    return {"stream_read_gbs": round(best, 1), "stream_read_bytes": total_bytes,
+            "per_launch_32mib_gbs": round(slice_bytes / us_slice / 1e3, 1), "per_launch_32mib_us": round(us_slice, 3),
+            "kernel": "si_read_bandwidth_probe (16-byte non-temporal loads, 8 blocks of 256 threads per CU)"}
 
 
 def graph_us(fn, calls, reps=4, warm=1):
@@ -282,50 +363,79 @@ def dense_torch_mlp(wg, wu, wd, x):
 
 
 def report_alpha(args, si, synth, dev):
-    """The 7B workload's alpha sweep: per alpha, us per fused call, kept
-    rows, algorithmic bytes and GB/s, active recall and the paper's
-    precision / recall of the predicted-sparse class (truth: which gate
-    pre-activations are positive, from a dense fp32 product on the device),
-    and the speedup over the same call at alpha = +inf (every row kept) and
-    over torch's dense fp16 GEMMs."""
+    """The 7B workload's alpha sweep with the actual-sparsity ablation (the
+    paper's +-AS comparison, Section V-B): two pools of 16 layers, the planted
+    one (gate signs disagree with the token with probability 0.4 on active
+    rows, 0.6 on inactive ones, so the prediction is certain) and an
+    uncertain one (0.47 / 0.53); per pool, flags (default, SI_NO_AS,
+    SI_NO_SPECULATION) and alpha: us per fused call, kept rows, the rows the
+    method needs (from the values) and the rows the kernel read (its
+    counters), algorithmic GB/s, active recall and the paper's precision /
+    recall of the predicted-sparse class (truth from a dense fp32 gate
+    product on the device), and the speedup over the dense call (alpha =
+    +inf with SI_NO_AS: every row of the three matrices read) and, for the
+    planted pool, over torch's dense fp16 GEMMs."""
     import torch
 
     from paper_2411_12692_amd import schedule
 
     L = args.layers
-    pls = [synth.planted_layer(D, K, S, config=2, layer=l, device=dev) for l in range(L)]
-    layers = [si.MLPLayer(p.w_gate, p.w_up, p.w_down, keep_w_down=True) for p in pls]
-    xs = [p.x for p in pls]
-    pos = [schedule.gate_positive(p.w_gate, p.x) for p in pls]
-    del pls
-    ys = [torch.empty(1, D, dtype=torch.float32, device=dev) for _ in range(L)]
-    dense_torch = graph_us(lambda i: dense_torch_mlp(layers[i % L].w_gate, layers[i % L].w_up,
-                                                     layers[i % L].w_down, xs[i % L]), 4 * L)
-    rows = []
-    for alpha in (0.7, 1.0, 1.03, 1.45, 1.5, math.inf):
-        kept, q = [], []
-        bsum = 0
-        for l in range(L):
-            _, (mask, _, _, cnt) = layers[l](xs[l], alpha, outputs=True)
-            c = cnt.tolist()
-            bsum += algorithmic_bytes(K, D, 1, *c)
-            kept.append(c[0])
-            q.append(schedule.quality(mask, pos[l]))
-        us = graph_us(lambda i: layers[i % L](xs[i % L], alpha, y=ys[i % L]), 4 * L, reps=16)
-        rows.append({"alpha": alpha, "us_per_layer": round(us, 3), "kept_rows_mean": sum(kept) / L,
-                     "bytes_per_layer": int(bsum / L), "gbs": round(bsum / L / us / 1e3, 1),
-                     "frac_of_peak": round(bsum / L / us / 1e3 / HBM_PEAK_GBS, 4),
-                     "active_recall": round(sum(x["active_recall"] for x in q) / L, 5),
-                     "missed_rows_total": sum(x["missed"] for x in q),
-                     "sparse_precision": round(sum(x["sparse_precision"] for x in q) / L, 5),
-                     "sparse_recall": round(sum(x["sparse_recall"] for x in q) / L, 5)})
-    dense = rows[-1]["us_per_layer"]
-    for r in rows:
-        r["speedup_vs_dense_call"] = round(dense / r["us_per_layer"], 2)
-        r["speedup_vs_torch_dense"] = round(dense_torch / r["us_per_layer"], 2)
-        r.update({"report": "alpha", "workload": f"7B-shaped layer d={D} k={K}, planted s={S}, batch 1, pool of {L}",
-                  "torch_dense_us": round(dense_torch, 3)})
-        print(json.dumps(r), flush=True)
+    pools = [("planted", 2, 0.4, 0.6, (0.7, 1.0, 1.03, 1.45, 1.5, math.inf)),
+             ("uncertain", 6, 0.47, 0.53, (0.9, 1.0, 1.03, 1.05, 1.1, 1.2, 1.35, 1.5, math.inf))]
+    flag_sets = (("default", 0), ("no_as", si.SI_NO_AS), ("no_speculation", si.SI_NO_SPECULATION))
+    for name, config, pa, pi, alphas in pools:
+        pls = [synth.planted_layer(D, K, S, config=config, layer=l, device=dev, p_active=pa, p_inactive=pi)
+               for l in range(L)]
+        layers = [si.MLPLayer(p.w_gate, p.w_up, p.w_down, keep_w_down=name == "planted") for p in pls]
+        xs = [p.x for p in pls]
+        gpos = [(p.x.float() @ p.w_gate.float().t())[0] > 0 for p in pls]
+        unz = [(p.x.float() @ p.w_up.float().t())[0] != 0 for p in pls]
+        pos = [schedule.gate_positive(p.w_gate, p.x) for p in pls]
+        del pls
+        ys = [torch.empty(1, D, dtype=torch.float32, device=dev) for _ in range(L)]
+        dense_torch = None
+        if name == "planted":
+            dense_torch = graph_us(lambda i: dense_torch_mlp(layers[i % L].w_gate, layers[i % L].w_up,
+                                                             layers[i % L].w_down, xs[i % L]), 4 * L)
+        for fname, flags in flag_sets:
+            rows = []
+            for alpha in alphas:
+                kept, q = [], []
+                need_sum, read_sum, bneed, bread = [0, 0, 0], [0, 0, 0], 0, 0
+                for l in range(L):
+                    _, (mask, _, _, cnt) = layers[l](xs[l], alpha, flags=flags, outputs=True)
+                    m = mask.bool()
+                    need = [int(m.sum()), int((m & gpos[l]).sum()), int((m & gpos[l] & unz[l]).sum())]
+                    rd = cnt.tolist()
+                    need_sum = [a + b for a, b in zip(need_sum, need)]
+                    read_sum = [a + b for a, b in zip(read_sum, rd)]
+                    bneed += algorithmic_bytes(K, D, 1, *need)
+                    bread += algorithmic_bytes(K, D, 1, *rd)
+                    kept.append(need[0])
+                    q.append(schedule.quality(mask, pos[l]))
+                us = graph_us(lambda i: layers[i % L](xs[i % L], alpha, flags=flags, y=ys[i % L]), 4 * L, reps=16)
+                rows.append({"alpha": alpha, "us_per_layer": round(us, 3), "kept_rows_mean": sum(kept) / L,
+                             "rows_needed_mean": [round(v / L, 1) for v in need_sum],
+                             "rows_read_mean": [round(v / L, 1) for v in read_sum],
+                             "bytes_per_layer": int(bneed / L), "bytes_read_per_layer": int(bread / L),
+                             "gbs": round(bneed / L / us / 1e3, 1),
+                             "frac_of_peak": round(bneed / L / us / 1e3 / HBM_PEAK_GBS, 4),
+                             "active_recall": round(sum(x["active_recall"] for x in q) / L, 5),
+                             "missed_rows_total": sum(x["missed"] for x in q),
+                             "sparse_precision": round(sum(x["sparse_precision"] for x in q) / L, 5),
+                             "sparse_recall": round(sum(x["sparse_recall"] for x in q) / L, 5)})
+            dense = rows[-1]["us_per_layer"]
+            for r in rows:
+                r["speedup_vs_dense_call"] = round(dense / r["us_per_layer"], 2)
+                if dense_torch is not None:
+                    r["speedup_vs_torch_dense"] = round(dense_torch / r["us_per_layer"], 2)
+                    r["torch_dense_us"] = round(dense_torch, 3)
+                r.update({"report": "alpha", "pool": name, "flags": fname,
+                          "workload": f"7B-shaped layer d={D} k={K}, planted s={S}, gate-sign disagreement "
+                                      f"{pa}/{pi} (active/inactive rows), batch 1, pool of {L}"})
+                print(json.dumps(r), flush=True)
+        del layers, xs
+        torch.cuda.empty_cache()
 
 
 def report_stacks(args, si, synth, dev):
@@ -394,10 +504,9 @@ def report_stacks(args, si, synth, dev):
         xs0 = [x.clone() for x in inputs[0]]
         counts = []
         for l in range(n_layers):
-            _, (_, _, _, c) = layers[l](xs0[l], 1.0, outputs=True)
-            counts.append(c)
+            _, (mask, _, _, _) = layers[l](xs0[l], 1.0, outputs=True)
+            counts.append(truth_counts(mask, xs0[l], layers[l].w_gate, layers[l].w_up))
         torch.cuda.synchronize()
-        counts = [c.tolist() for c in counts]
         bytes_token = sum(algorithmic_bytes(k, d, 1, *c) for c in counts)
 
         def timed_tokens(mlp):
@@ -502,9 +611,9 @@ def report_sweep(args, si, synth, dev):
         for b in (1, 2, 4, 8):
             xs = [synth.batch_tokens(p, b, config=5, layer_id=l) for l, p in enumerate(pls)]
             ms = [synth.batch_union_mask(p, b, config=5, layer_id=l) for l, p in enumerate(pls)]
-            cnts = [layers[l].sparse_mlp(xs[l], mask=ms[l], counters=True)[1] for l in range(L)]
+            cnts = [truth_counts(ms[l], xs[l], layers[l].w_gate, layers[l].w_up) for l in range(L)]
             torch.cuda.synchronize()
-            bsum = sum(algorithmic_bytes(K, D, b, *c.tolist()) for c in cnts)
+            bsum = sum(algorithmic_bytes(K, D, b, *c) for c in cnts)
             sp = graph_us(lambda i: layers[i % L].sparse_mlp(xs[i % L], mask=ms[i % L]), 4 * L, reps=8)
             dn = graph_us(lambda i: layers[i % L].sparse_mlp(xs[i % L], mask=ones), 4 * L, reps=8)
             tdn = graph_us(lambda i: dense_torch_mlp(layers[i % L].w_gate, layers[i % L].w_up, layers[i % L].w_down,
@@ -637,26 +746,46 @@ def main():
             return layers[l].block(hs[l], nws[l], EPS, args.alpha, outputs=outputs, y=ys[l])
         return layers[l](xs[l], args.alpha, outputs=outputs, y=ys[l])
 
-    # per-layer work counters (deterministic per layer) -> algorithmic bytes
-    counts = []
+    # per layer (each layer's call is deterministic): the kept rows, the rows
+    # the kernel read (its counters, speculative requests included) and the
+    # rows the method needs (from the values) -> algorithmic bytes
+    counts, reads = [], []
     for l in range(L):
-        _, (_, _, _, c) = step(l, outputs=True)
-        counts.append(c)
+        _, (mask, _, _, c) = step(l, outputs=True)
+        reads.append(c)
+        if int8:
+            lay = layers[l]
+            wg_v = lay.q_gate.float() * lay.s_gate[:, None]
+            wu_v = lay.q_up.float() * lay.s_up[:, None]
+        else:
+            wg_v, wu_v = layers[l].w_gate, layers[l].w_up
+        if block:  # the kernel's input: fp16(RMSNorm(h) * norm_w)
+            hh = hs[l]
+            xv = (hh * torch.rsqrt((hh * hh).mean(dim=-1, keepdim=True) + EPS) * nws[l]).half()
+        else:
+            xv = xs[l]
+        counts.append(truth_counts(mask, xv, wg_v, wu_v))
+        del wg_v, wu_v
     torch.cuda.synchronize()
-    counts = [c.tolist() for c in counts]
+    reads = [c.tolist() for c in reads]
     if args.profile_pass:
         profile_pass(step, L, max(args.launches, L), dev)
         return
     bytes_per_layer = [algorithmic_bytes(K_, D_, 1, *c, block=block, int8=int8) for c in counts]
     mean_bytes = sum(bytes_per_layer) / L
+    read_bytes = sum(algorithmic_bytes(K_, D_, 1, *c, block=block, int8=int8) for c in reads) / L
 
-    us_per_layer, steps, warmup, wall_us = time_graph(step, L, args.steps, args.warmup)
-    print(f"# timed {steps} steps: {us_per_layer:.3f} us/layer (wall {wall_us:.3f})", file=sys.stderr, flush=True)
+    steps, warmup = args.steps, args.warmup
+    us_per_layer, wall_us = time_steps(step, steps, warmup)
+    print(f"# timed {steps} steps after {warmup} warm-up steps: {us_per_layer:.3f} us/layer (wall {wall_us:.3f})",
+          file=sys.stderr, flush=True)
     plain_us = None
     if block:  # the same layers through the plain call (x given, no residual), for comparison
-        plain_us, _, _, _ = time_graph(lambda i: layers[i % L](xs[i % L], args.alpha, y=ys[i % L]), L,
-                                       args.steps, args.warmup)
+        plain_us, _ = time_steps(lambda i: layers[i % L](xs[i % L], args.alpha, y=ys[i % L]), steps, warmup)
         print(f"# plain call on the same layers: {plain_us:.3f} us/layer", file=sys.stderr, flush=True)
+    peak = measured_read_peak(si, dev) if not args.no_peak else None
+    if peak:
+        print(f"# streaming-read probe: {peak}", file=sys.stderr, flush=True)
 
     # The timed graph holds nothing but k_owned launches on one stream, so the
     # per-step time above is that kernel's average launch duration.
@@ -703,7 +832,10 @@ def main():
                         f"HIP-graph replay",
             "d": D_, "k": K_, "batch": 1, "alpha": args.alpha, "layers_in_pool": L,
             "kept_rows": [c[0] for c in counts[:4]],
+            "rows_needed": [c for c in counts[:2]],
+            "rows_read": [c for c in reads[:2]],
             "bytes_per_layer": int(mean_bytes),
+            "bytes_read_per_layer": int(read_bytes),
         },
         "roofline": {
             "kernel": "k_owned (predict + group exchange + gate/up + down, one launch per layer)",
@@ -718,6 +850,9 @@ def main():
             "isolated_launch_us": round(isolated_us, 3),
         },
     }
+    if peak:
+        result["measured_peak"] = peak
+        result["roofline"]["frac_of_measured_peak"] = round(achieved / peak["stream_read_gbs"], 4)
     if plain_us is not None:
         result["plain_call_us"] = round(plain_us, 3)
     if not args.no_cpu_baseline:

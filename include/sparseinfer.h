@@ -27,6 +27,17 @@
  *   the next (it resets its own counters), so it must not be modified by the
  *   caller afterwards, and one workspace must not be used by two calls that
  *   can run at the same time (e.g. on two streams).
+ * - Co-residency: where si_single_launch(k, d, b) is 1, a call is one kernel
+ *   of one block per compute unit whose blocks hand each other data while it
+ *   runs, so every block must be resident at once.  The call needs every
+ *   compute unit of the device to itself: a kernel running concurrently on
+ *   another stream, or a CU mask that hides compute units, can keep a block
+ *   from starting.  Every wait inside the kernel is bounded (on the order of
+ *   a millisecond); a wait that gives up lets the call finish with wrong
+ *   results and sets a sticky error word in the workspace.  From then on the
+ *   single-launch calls on that workspace compute nothing and fill y with NaN
+ *   until si_workspace_check() has reported the error (SI_ERR_TIMEOUT) and
+ *   reset the workspace.
  */
 #ifndef SPARSEINFER_H
 #define SPARSEINFER_H
@@ -47,8 +58,11 @@ typedef enum {
   SI_ERR_WORKSPACE = 5, /* workspace smaller than si_workspace_bytes()     */
   SI_ERR_HIP = 6,       /* the HIP runtime reported an error               */
   SI_ERR_FLAGS = 7,     /* unknown bits in `flags`                         */
-  SI_ERR_ARG = 8        /* another argument out of range (eps, overlapping
+  SI_ERR_ARG = 8,       /* another argument out of range (eps, overlapping
                            buffers)                                        */
+  SI_ERR_TIMEOUT = 9,   /* a bounded wait inside a kernel gave up (blocks of
+                           a single-launch call were not all resident)     */
+  SI_ERR_LIST = 10      /* a caller's active_idx held a row outside [0, k) */
 } si_status;
 
 /* Flags of si_sparse_mlp / si_predict_sparse_mlp. */
@@ -112,6 +126,60 @@ int32_t si_alpha_threshold(float alpha, int d);
 /* Bytes of workspace needed by si_predict / si_sparse_mlp /
  * si_predict_sparse_mlp for these shapes (0 for unsupported shapes). */
 size_t si_workspace_bytes(int k, int d, int b);
+
+/*
+ * Errors found inside kernels, which no call can return when it is made
+ * (calls only enqueue work).  Waits for `stream` (NULL: the default
+ * stream), then reads the workspace's sticky error word:
+ *   SI_OK          : no error since the workspace was zero-filled or last
+ *                    checked;
+ *   SI_ERR_TIMEOUT : a bounded wait gave up (see "Co-residency" above); the
+ *                    results of that call and of the single-launch calls on
+ *                    this workspace since then are wrong (y is NaN);
+ *   SI_ERR_LIST    : a caller's active_idx held a row outside [0, k) (the
+ *                    entry was skipped).
+ * On an error the whole workspace (workspace_bytes bytes) is zero-filled,
+ * which restores it to its first-use state, and later calls compute again.
+ * Not for use during stream capture (it synchronizes).  SI_ERR_NULL /
+ * SI_ERR_ALIGN for a bad pointer, SI_ERR_HIP if the synchronization or a
+ * copy fails.
+ */
+si_status si_workspace_check(void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Host-only: the status that si_workspace_check() returns for the value
+ * `bits` of the sticky error word (bit 0: a wait gave up, bit 2: a list row
+ * outside [0, k); a wait that gave up takes precedence).  Unknown bits give
+ * SI_ERR_ARG.  Needs no GPU.
+ */
+si_status si_device_error_status(uint32_t bits);
+
+/*
+ * Diagnostic read-back, for tests: the per-row values h3_i,t of Eq. (1)
+ * step 3 (h3 = ReLU(W_gate,i . x_t) * (W_up,i . x_t); ReLU(W_fc1,i . x_t)
+ * for the non-gated MLP; with the INT8 scales applied) that the last MLP
+ * call made with this workspace computed.
+ *   mask : [k] uint8, the rows that call kept (nonzero = kept), read.
+ *   h3   : [k][b] float32, written: the call's value for each kept row, 0 for
+ *          the other rows, NaN for a kept row for which the call left no
+ *          value of its own (a row it dropped).
+ *   b    : the batch of that call.
+ * The MLP call must be the last call made with the workspace (a later
+ * si_predict replaces what it left).  Enqueued on `stream`.
+ */
+si_status si_read_h3(const void* workspace, size_t workspace_bytes, int k, int d, int b, const uint8_t* mask,
+                     float* h3, void* stream);
+
+/*
+ * Diagnostic, outside the path: read `bytes` bytes of device memory at `buf`
+ * (16-byte aligned, bytes a positive multiple of 16) once, with 16-byte
+ * non-temporal loads from a grid of 8 blocks of 256 threads per compute unit.
+ * The time it takes gives the streaming-read bandwidth the device achieves,
+ * which the benchmark reports beside the HBM peak.  `sink` ([1] uint32) is
+ * written only if the XOR of the data equals one fixed constant (so that the
+ * loads cannot be dropped).  Enqueued on `stream`.
+ */
+si_status si_read_bandwidth_probe(const void* buf, size_t bytes, uint32_t* sink, void* stream);
 
 /*
  * Predict the rows of W_gate whose ReLU output will be zero (Section IV-A).

@@ -18,7 +18,7 @@ from ._lib import SI_NO_AS, SI_NO_SPECULATION, SparseInferError
 
 __all__ = [
     "SI_NO_AS", "SI_NO_SPECULATION", "SparseInferError", "signs_bytes", "alpha_threshold", "workspace_bytes",
-    "new_workspace", "pack_signs", "signs_to_canonical", "transpose_down", "predict",
+    "new_workspace", "workspace_check", "read_h3", "pack_signs", "signs_to_canonical", "transpose_down", "predict",
     "sparse_mlp", "predict_sparse_mlp", "mlp_block", "MLPLayer",
     "quantize_rows_i8", "pack_signs_i8", "transpose_down_i8", "sparse_mlp_i8", "predict_sparse_mlp_i8",
     "Int8MLPLayer",
@@ -69,6 +69,24 @@ def new_workspace(k: int, d: int, b: int = 1, device=None) -> torch.Tensor:
     if n == 0:
         raise ValueError(f"unsupported shape k={k} d={d} b={b}")
     return torch.zeros(n, dtype=torch.uint8, device=device or "cuda")
+
+
+def workspace_check(workspace: torch.Tensor, stream=None) -> int:
+    """``si_workspace_check``: waits for the stream, returns the status of the
+    workspace's sticky device error word (``SI_OK``, ``SI_ERR_TIMEOUT`` or
+    ``SI_ERR_LIST``) and resets the workspace when it is not ``SI_OK``."""
+    st = stream if stream is not None else _stream()
+    return int(_lib.status("si_workspace_check", _vp(workspace), workspace.numel(), st))
+
+
+def read_h3(workspace: torch.Tensor, k: int, d: int, b: int, mask: torch.Tensor) -> torch.Tensor:
+    """``si_read_h3``: the per-row h3 (Eq. (1) step 3) of the last MLP call
+    made with ``workspace``, ``[k][b]`` float32 (0 off ``mask``, NaN for a
+    kept row the call left no value for)."""
+    _dev(mask, "mask", (torch.uint8,), 1)
+    out = torch.empty(k, b, dtype=torch.float32, device=mask.device)
+    _lib.call("si_read_h3", _vp(workspace), workspace.numel(), k, d, b, _vp(mask), _vp(out), _stream())
+    return out
 
 
 def pack_signs(w_gate: torch.Tensor) -> torch.Tensor:

@@ -21,6 +21,8 @@ SI_ERR_WORKSPACE = 5
 SI_ERR_HIP = 6
 SI_ERR_FLAGS = 7
 SI_ERR_ARG = 8
+SI_ERR_TIMEOUT = 9
+SI_ERR_LIST = 10
 SI_NO_AS = 1
 SI_NO_SPECULATION = 2
 
@@ -40,6 +42,10 @@ SIGNATURES = {
     "si_transpose_down": (_i, [_p, _i, _i, _p, _p]),
     "si_alpha_threshold": (ctypes.c_int32, [_f, _i]),
     "si_workspace_bytes": (_sz, [_i, _i, _i]),
+    "si_workspace_check": (_i, [_p, _sz, _p]),
+    "si_device_error_status": (_i, [_u32]),
+    "si_read_h3": (_i, [_p, _sz, _i, _i, _i, _p, _p, _p]),
+    "si_read_bandwidth_probe": (_i, [_p, _sz, _p, _p]),
     "si_single_launch": (_i, [_i, _i, _i]),
     "si_predict": (_i, [_p, _i, _i, _p, _i, _f, _p, _p, _p, _p, _sz, _p]),
     "si_sparse_mlp": (_i, [_p, _p, _p, _i, _i, _p, _i, _p, _p, _p, _p, _p, _sz, _u32, _p, _p]),

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsparseinfer.so")
-SOURCES = ["api.hip", "pack.hip", "predict.hip", "mlp.hip", "layer.hip", "owned.hip"]
+SOURCES = ["api.hip", "pack.hip", "predict.hip", "mlp.hip", "layer.hip", "owned.hip", "diag.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc" if os.path.exists("/opt/rocm/bin/hipcc") else "hipcc")

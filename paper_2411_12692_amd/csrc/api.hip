@@ -92,6 +92,54 @@ size_t si_workspace_bytes(int k, int d, int b) {
   return si::ws_layout(k, b).total;
 }
 
+si_status si_device_error_status(uint32_t bits) {
+  if (bits == 0) return SI_OK;
+  if (bits & ~(si::kErrLookbackSpin | si::kErrRow)) return fail(SI_ERR_ARG, "unknown device error bits 0x%x", bits);
+  if (bits & si::kErrLookbackSpin)
+    return fail(SI_ERR_TIMEOUT, "a wait inside a kernel gave up: not every block of a single-launch call was resident");
+  return fail(SI_ERR_LIST, "a caller's active_idx held a row outside [0, k)");
+}
+
+si_status si_workspace_check(void* workspace, size_t workspace_bytes, void* stream) {
+  REQUIRE_PTR(workspace);
+  REQUIRE_ALIGNED(workspace);
+  if (workspace_bytes < si::H_WORDS * sizeof(uint32_t))
+    return fail(SI_ERR_WORKSPACE, "workspace of %zu bytes is smaller than its header", workspace_bytes);
+  hipStream_t st = (hipStream_t)stream;
+  if (si_status s = hip_status(hipStreamSynchronize(st), "stream synchronize")) return s;
+  uint32_t bits = 0;
+  const uint32_t* hdr = static_cast<const uint32_t*>(workspace);
+  if (si_status s = hip_status(hipMemcpy(&bits, hdr + si::H_ERR, sizeof bits, hipMemcpyDeviceToHost), "read error word"))
+    return s;
+  const si_status st_bits = si_device_error_status(bits);
+  if (st_bits == SI_OK) return SI_OK;
+  char msg[sizeof g_err];
+  snprintf(msg, sizeof msg, "%s", g_err);
+  if (si_status s = hip_status(hipMemsetAsync(workspace, 0, workspace_bytes, st), "workspace reset")) return s;
+  if (si_status s = hip_status(hipStreamSynchronize(st), "stream synchronize")) return s;
+  return fail(st_bits, "%s (the workspace has been reset)", msg);
+}
+
+si_status si_read_h3(const void* workspace, size_t workspace_bytes, int k, int d, int b, const uint8_t* mask,
+                     float* h3, void* stream) {
+  REQUIRE_PTR(mask);
+  REQUIRE_PTR(h3);
+  REQUIRE_ALIGNED(mask);
+  REQUIRE_ALIGNED(h3);
+  if (si_status s = check_kd(k, d)) return s;
+  if (si_status s = check_b(b)) return s;
+  if (si_status s = check_ws(workspace, workspace_bytes, k, b)) return s;
+  return hip_status(si::launch_read_h3(workspace, k, b, mask, h3, (hipStream_t)stream), "read_h3 launch");
+}
+
+si_status si_read_bandwidth_probe(const void* buf, size_t bytes, uint32_t* sink, void* stream) {
+  REQUIRE_PTR(buf);
+  REQUIRE_PTR(sink);
+  REQUIRE_ALIGNED(buf);
+  if (bytes == 0 || bytes % 16 != 0) return fail(SI_ERR_SHAPE, "bytes=%zu must be a positive multiple of 16", bytes);
+  return hip_status(si::launch_read_probe(buf, bytes, sink, (hipStream_t)stream), "read probe launch");
+}
+
 int si_single_launch(int k, int d, int b) {
   if (check_kd(k, d) != SI_OK || check_b(b) != SI_OK) return 0;
   return si::layer_supported(k, d, b) && si::owned_supported(k, d, b) ? 1 : 0;

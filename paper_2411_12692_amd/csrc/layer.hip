@@ -90,7 +90,7 @@ struct LayerLds {
   float hs[kDownRound * BM];      // h3 of the down round's positions
   int sc[8];                      // block scalars: lo, hi, dlo, dhi
   int n_late, n_up, n_down, zok;
-  uint32_t epoch;
+  uint32_t epoch, err;
 };
 
 template <int BM, int NU>
@@ -129,7 +129,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
       const u32x4 xv = xg[min(t * U + u, nx - 1)];
       if (i == tid && tid == 0) {
         asm volatile("" ::: "memory");
-        L.epoch = ld_agent(&a.hdr[H_EPOCH]);
+        load_epoch(a.hdr, L.epoch, L.err);
         L.n_up = 0;
         L.n_down = 0;
         L.zok = 0;
@@ -146,6 +146,20 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
     }
   }
   __syncthreads();
+  // a workspace left inconsistent by a call whose bounded wait gave up (its
+  // sticky error word is set): nothing is computed until the workspace is
+  // reset, and the owners of the tiles of y fill them with NaN (each thread
+  // the columns it zeroed above)
+  if (uniform(L.err) & kErrLookbackSpin) {
+    if (owns_tile) {
+      for (int i = tid; i < b * kTile; i += kLThreads) {
+        const int t = i / kTile, col = blk * kTile + (i - t * kTile);
+        if (col < d)
+          __hip_atomic_store(&a.y[(size_t)t * d + col], __builtin_nanf(""), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    return;
+  }
   const uint32_t epoch = uniform(L.epoch);
   const uint32_t tag = epoch_tag(epoch);
   if (tid == 0) st_agent64(&a.alive[blk], tagged(tag, 0u));  // this block has read the call counter
@@ -430,6 +444,7 @@ __global__ __launch_bounds__(kLThreads) void k_layer(LayerArgs a) {
   if (tid == 0) {
     a.counts[2 * blk] = L.n_up;
     a.counts[2 * blk + 1] = L.n_down;
+    if (blk == 0) a.hdr[H_H3_FORM] = kH3ByPos;
   }
 }
 
@@ -470,21 +485,20 @@ hipError_t launch_sum_counts(const int32_t* counts, int slots, const int32_t* n_
 // kernel's LDS does not fit or it cannot be resident on every CU.
 template <int BM, int NU>
 static int layer_blocks() {
-  static int blocks = -1;
-  if (blocks < 0) {
-    blocks = 0;
+  static std::atomic<int> cache[kMaxDevices];
+  return per_device_once(cache, [](int dev) -> int {
     constexpr int lds = layer_lds_bytes<BM, NU>();
-    if constexpr (lds <= kMaxLds) {
-      int dev = 0, cus = 0, per_cu = 0;
+    if constexpr (lds > kMaxLds) {
+      return 0;
+    } else {
+      int cus = 0, per_cu = 0;
       const void* fn = reinterpret_cast<const void*>(&k_layer<BM, NU>);
-      if (hipGetDevice(&dev) != hipSuccess) return 0;
-      if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-      if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return 0;
-      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kLThreads, lds) != hipSuccess) return 0;
-      if (per_cu >= 1) blocks = cus < kMaxLayerBlocks ? cus : kMaxLayerBlocks;
+      if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
+      if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return -1;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kLThreads, lds) != hipSuccess) return -1;
+      return per_cu >= 1 ? (cus < kMaxLayerBlocks ? cus : kMaxLayerBlocks) : 0;
     }
-  }
-  return blocks;
+  });
 }
 
 template <int BM, int NU>

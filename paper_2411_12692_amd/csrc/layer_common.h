@@ -108,7 +108,29 @@ __device__ inline void wait_alive(const uint64_t* alive, int blocks, int t, int 
 }
 
 // Block 0, once every block has read the call counter: advance it.
+// After a wait that gave up the counter is still advanced: otherwise the next
+// call would carry this call's tag and take every word this call published as
+// its own.  A late block may still tag its words for the next call, so the
+// workspace is marked inconsistent (the sticky error word) until reset.
 __device__ inline void advance_epoch(uint32_t* hdr, uint32_t epoch) { st_agent(&hdr[H_EPOCH], epoch + 1u); }
+
+// The call counter and the sticky error word, in one request.
+__device__ inline void load_epoch(const uint32_t* hdr, uint32_t& epoch, uint32_t& err) {
+  const uint64_t w = ld_agent64(reinterpret_cast<const uint64_t*>(hdr));
+  epoch = (uint32_t)w;
+  err = (uint32_t)(w >> 32);
+}
+
+// A block's tile of y filled with NaN (one wave: lane = pair of columns).
+__device__ inline void poison_tile(float* y, int b, int d, int tile, int lane) {
+  const int half_cols = min(kTile, d - tile * kTile) / 2;
+  const float nan = __builtin_nanf("");
+  const uint64_t v = ((uint64_t)__float_as_uint(nan) << 32) | __float_as_uint(nan);
+  for (int t = 0; t < b; ++t) {
+    uint64_t* yt = reinterpret_cast<uint64_t*>(y + (size_t)t * d + tile * kTile);
+    for (int c = lane; c < half_cols; c += kWave) st_agent64(yt + c, v);
+  }
+}
 
 // Dot products of a row held as NU 16-byte units per lane (unit lane + 64 j)
 // with the BM tokens in LDS (token t at xs[t * NU * 64], a compile-time

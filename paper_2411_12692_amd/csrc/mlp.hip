@@ -36,6 +36,7 @@ __global__ __launch_bounds__(256) void k_gate_up(const u32x4* __restrict__ wg, c
   const int U = d >> 3;
   if (blockIdx.x == 0) {  // y is accumulated with atomics by k_down
     for (int i = tid; i < B * d; i += 256) y[i] = 0.f;
+    if (tid == 0) hdr[H_H3_FORM] = kH3PlainByRow;
   }
   const int n = min(max(*n_ptr, 0), k);
   if ((int)blockIdx.x * 4 >= n) {
@@ -175,14 +176,13 @@ static hipError_t gate_up_b(const uint16_t* w_gate, const uint16_t* w_up, int k,
   const WsLayout L = ws_layout(k, B);
   char* base = static_cast<char*>(ws);
   const size_t lds = (size_t)B * d * sizeof(uint16_t);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gate_up<B>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)((size_t)kMaxB * kMaxD * sizeof(uint16_t)));
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  // the kernel's dynamic LDS limit, set once per device
+  static std::atomic<int> attr_set[kMaxDevices];
+  const int ok = per_device_once(attr_set, [](int) -> int {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_gate_up<B>), hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)((size_t)kMaxB * kMaxD * sizeof(uint16_t))) == hipSuccess ? 1 : -1;
+  });
+  if (ok != 1) return hipErrorInvalidConfiguration;
   int blocks = (k + 3) / 4;
   if (blocks > kGateUpMaxBlocks) blocks = kGateUpMaxBlocks;
   *slots = blocks;

@@ -137,7 +137,7 @@ struct OwnedLds {
   int wsum[kOW];
   float nsum[kOW][kMaxB];  // decoder-block mode: per-wave sums of squares of the tokens
   int n_own, n_up, n_down;
-  uint32_t epoch;
+  uint32_t epoch, err;
 };
 
 template <int BM, int NU>
@@ -465,7 +465,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       const u32x4 xv = xg[min(i, U - 1)];
       if (i == tid && tid == 0) {
         asm volatile("" ::: "memory");
-        L.epoch = ld_agent(&a.hdr[H_EPOCH]);
+        load_epoch(a.hdr, L.epoch, L.err);
         L.n_up = 0;
         L.n_down = 0;
       }
@@ -486,7 +486,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
     if (tid == 0) {
       asm volatile("" ::: "memory");
-      L.epoch = ld_agent(&a.hdr[H_EPOCH]);
+      load_epoch(a.hdr, L.epoch, L.err);
       L.n_up = 0;
       L.n_down = 0;
     }
@@ -538,7 +538,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
     if (tid == 0) {
       asm volatile("" ::: "memory");
-      L.epoch = ld_agent(&a.hdr[H_EPOCH]);
+      load_epoch(a.hdr, L.epoch, L.err);
       L.n_up = 0;
       L.n_down = 0;
     }
@@ -549,6 +549,13 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
   }
   __syncthreads();
+  // a workspace left inconsistent by a call whose bounded wait gave up (its
+  // sticky error word is set): nothing is computed until the workspace is
+  // reset, and the owners of the tiles of y fill them with NaN
+  if (uniform(L.err) & kErrLookbackSpin) {
+    if (owns_tile && wv == kTileWave) poison_tile(a.y, b, d, blk, lane);
+    return;
+  }
   if constexpr (block_mode && !kKeep) scale_x();  // h and norm_w read again: before the counts, not behind the publishing stores
   const uint32_t epoch = uniform(L.epoch);
   const uint32_t tag = epoch_tag(epoch);
@@ -1034,6 +1041,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     const int before = block_sum(L, sum, lane, wv);
     for (int q = tid; q < n_own; q += kOT) a.idx[before + q] = (int32_t)(L.srow[q] & 0x7fffffffu);
   }
+  if (a.mlp && blk == 0 && tid == 0) a.hdr[H_H3_FORM] = kH3ByRow;
   SI_TRACE_MARK(10);
   SI_TRACE_FLUSH;
 }
@@ -1047,23 +1055,24 @@ static int owned_rows_per_block(int k, int P, int tiles) {
   return (R + 7) / 8 * 8;
 }
 
+// Grid of the row-owning kernel on the current device: one block per compute
+// unit, or 0 if its LDS does not fit or one block cannot be resident per CU.
 template <int BM, int NU, int MODE = kModePlain>
 static int owned_blocks() {
-  static int blocks = -1;
-  if (blocks < 0) {
-    blocks = 0;
+  static std::atomic<int> cache[kMaxDevices];
+  return per_device_once(cache, [](int dev) -> int {
     constexpr int lds = owned_lds_bytes<BM, NU>();
-    if constexpr (lds <= kMaxLds) {
-      int dev = 0, cus = 0, per_cu = 0;
+    if constexpr (lds > kMaxLds) {
+      return 0;
+    } else {
+      int cus = 0, per_cu = 0;
       const void* fn = reinterpret_cast<const void*>(&k_owned<BM, NU, MODE>);
-      if (hipGetDevice(&dev) != hipSuccess) return 0;
-      if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-      if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return 0;
-      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kOT, lds) != hipSuccess) return 0;
-      if (per_cu >= 1) blocks = cus < kMaxLayerBlocks ? cus : kMaxLayerBlocks;
+      if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
+      if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return -1;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kOT, lds) != hipSuccess) return -1;
+      return per_cu >= 1 ? (cus < kMaxLayerBlocks ? cus : kMaxLayerBlocks) : 0;
     }
-  }
-  return blocks;
+  });
 }
 
 template <int BM, int NU>

@@ -90,6 +90,7 @@ __global__ __launch_bounds__(kPredWaves * kWave) void k_rows(
 
   if (FUSED && v == 0) {  // y is accumulated with atomics by the down-projection kernel
     for (int i = tid; i < B * d; i += NT) y[i] = 0.f;
+    if (tid == 0) hdr[H_H3_FORM] = kH3PlainByRow;
   }
   // 1. tokens -> LDS, then their packed sign words
   for (int i = tid; i < B * U; i += NT) xs[i] = reinterpret_cast<const u32x4*>(x)[i];
@@ -186,14 +187,13 @@ static hipError_t rows_b(const uint32_t* signs, int k, int d, const uint16_t* x,
   const WsLayout L = ws_layout(k, B);
   char* base = static_cast<char*>(ws);
   const size_t lds = (size_t)B * d * sizeof(uint16_t);
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_rows<B, FUSED>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)((size_t)kMaxB * kMaxD * sizeof(uint16_t)));
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
+  // the kernel's dynamic LDS limit, set once per device
+  static std::atomic<int> attr_set[kMaxDevices];
+  const int ok = per_device_once(attr_set, [](int) -> int {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_rows<B, FUSED>), hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)((size_t)kMaxB * kMaxD * sizeof(uint16_t))) == hipSuccess ? 1 : -1;
+  });
+  if (ok != 1) return hipErrorInvalidConfiguration;
   k_rows<B, FUSED><<<row_groups(k), kPredWaves * kWave, lds, s>>>(
       reinterpret_cast<const u32x4*>(signs), k, d, x, T, mask, idx, n_out,
       reinterpret_cast<uint64_t*>(base + L.status), reinterpret_cast<uint32_t*>(base),

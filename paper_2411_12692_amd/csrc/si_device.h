@@ -18,13 +18,19 @@ constexpr int kTile = 512;      // columns of y handled by one down-projection b
 // Header words at the start of the workspace.
 enum : int {
   H_EPOCH = 0,        // call counter: every predictor or layer call advances it once
-  H_ERR = 1,          // sticky device-side error bits
+  H_ERR = 1,          // sticky device-side error bits (read together with H_EPOCH as one 64-bit word)
   H_N_INTERNAL = 2,   // kept-row count when the list lives in the workspace
+  H_H3_FORM = 3,      // where the last MLP call left its per-row h3 values (kH3*)
   H_WORDS = 64
 };
 
 constexpr uint32_t kErrLookbackSpin = 1u;  // a look-back wait hit its spin limit
 constexpr uint32_t kErrRow = 4u;           // kept-row index outside [0, k)
+
+// Where the last MLP call left h3 (Eq. (1) step 3) in the workspace.
+constexpr uint32_t kH3ByRow = 1u;       // h3e[row][b]: this call's tag | fp32 bits
+constexpr uint32_t kH3ByPos = 2u;       // h3e[list position][b]: this call's tag | fp32 bits
+constexpr uint32_t kH3PlainByRow = 3u;  // h3[row][b] fp32, valid on the kept rows
 
 constexpr int kGateUpMaxBlocks = 2048;     // grid cap of the list-driven gate/up kernel
 constexpr int kMaxLayerBlocks = 1024;      // grid cap of the single-kernel path

@@ -5,7 +5,28 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace si {
+
+constexpr int kMaxDevices = 64;
+
+// A value computed once per device on first use there (grid sizes, kernel
+// attributes): computed into a local and published with one atomic store, so
+// that concurrent first calls from several host threads each compute the same
+// value and none reads a half-made one.  `compute(dev)` runs with `dev`
+// current and returns -1 on a HIP error (nothing is cached, 0 is returned).
+template <class F>
+inline int per_device_once(std::atomic<int> (&cache)[kMaxDevices], F compute) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+  const int c = cache[dev].load(std::memory_order_acquire);
+  if (c != 0) return c - 1;
+  const int v = compute(dev);
+  if (v < 0) return 0;
+  cache[dev].store(v + 1, std::memory_order_release);
+  return v;
+}
 
 hipError_t launch_pack_signs(const uint16_t* w_gate, int k, int d, uint32_t* signs, hipStream_t s);
 hipError_t launch_signs_to_canonical(const uint32_t* signs, int k, int d, uint32_t* out, hipStream_t s);
@@ -73,6 +94,13 @@ hipError_t launch_layer(const LayerCall& c, hipStream_t s);
 // NULL.  Only valid when owned_supported(k, d, b).
 bool owned_supported(int k, int d, int b);
 hipError_t launch_owned(const LayerCall& c, hipStream_t s);
+
+// Per-row h3 of the last MLP call made with workspace `ws` -> out[k][b]
+// (kept rows of `mask`; 0 elsewhere; NaN where the call left no value).
+hipError_t launch_read_h3(const void* ws, int k, int b, const uint8_t* mask, float* out, hipStream_t s);
+
+// Streaming read of `bytes` (a multiple of 16) at `buf` (diagnostic).
+hipError_t launch_read_probe(const void* buf, size_t bytes, uint32_t* sink, hipStream_t s);
 
 // mask -> ascending kept list and count (single block).
 hipError_t launch_compact(const uint8_t* mask, int k, int32_t* idx, int32_t* n_out, hipStream_t s);

@@ -135,3 +135,38 @@ def test_validation_errors(lib):
         st = _lib.status(name, *args)
         assert st == want, (name, args, st, _lib.last_error())
         assert _lib.last_error() != ""
+
+
+def test_device_error_status_mapping(lib):
+    """The sticky error word of a workspace -> the status si_workspace_check
+    returns: 0 -> OK, bit 0 (a wait gave up) -> TIMEOUT (over any other bit),
+    bit 2 (a list row outside [0, k)) -> LIST, unknown bits -> ARG."""
+    assert lib.si_device_error_status(0) == _lib.SI_OK
+    assert lib.si_device_error_status(1) == _lib.SI_ERR_TIMEOUT
+    assert lib.si_device_error_status(4) == _lib.SI_ERR_LIST
+    assert lib.si_device_error_status(5) == _lib.SI_ERR_TIMEOUT
+    for bad in (2, 8, 0x80000000, 0xFFFFFFFF):
+        assert lib.si_device_error_status(bad) == _lib.SI_ERR_ARG, bad
+    assert "resident" in (lib.si_device_error_status(1) and _lib.last_error())
+
+
+def test_workspace_check_and_read_h3_validation(lib):
+    ws = lib.si_workspace_bytes(128, 256, 1)
+    cases = [
+        ("si_workspace_check", (None, ws, None), _lib.SI_ERR_NULL),
+        ("si_workspace_check", (_p(A + 8), ws, None), _lib.SI_ERR_ALIGN),
+        ("si_workspace_check", (_p(A), 255, None), _lib.SI_ERR_WORKSPACE),
+        ("si_read_h3", (_p(A), ws, 128, 256, 1, None, _p(A), None), _lib.SI_ERR_NULL),
+        ("si_read_h3", (_p(A), ws, 128, 256, 1, _p(A), None, None), _lib.SI_ERR_NULL),
+        ("si_read_h3", (_p(A), ws, 128, 256, 9, _p(A), _p(A), None), _lib.SI_ERR_SHAPE),
+        ("si_read_h3", (_p(A), ws - 1, 128, 256, 1, _p(A), _p(A), None), _lib.SI_ERR_WORKSPACE),
+        ("si_read_h3", (None, ws, 128, 256, 1, _p(A), _p(A), None), _lib.SI_ERR_NULL),
+        ("si_read_bandwidth_probe", (None, 1024, _p(A), None), _lib.SI_ERR_NULL),
+        ("si_read_bandwidth_probe", (_p(A), 1024, None, None), _lib.SI_ERR_NULL),
+        ("si_read_bandwidth_probe", (_p(A + 4), 1024, _p(A), None), _lib.SI_ERR_ALIGN),
+        ("si_read_bandwidth_probe", (_p(A), 1000, _p(A), None), _lib.SI_ERR_SHAPE),
+        ("si_read_bandwidth_probe", (_p(A), 0, _p(A), None), _lib.SI_ERR_SHAPE),
+    ]
+    for name, args, want in cases:
+        st = _lib.status(name, *args)
+        assert st == want, (name, args, st, _lib.last_error())

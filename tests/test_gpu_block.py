@@ -16,6 +16,7 @@ import torch
 
 import oracle
 import paper_2411_12692_amd as si
+from h3check import check_h3, fp16_rows, workspace_ok
 from paper_2411_12692_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -54,9 +55,14 @@ class BlockCase:
 
     def check(self, alpha, flags=0):
         y, mask, idx, n, cnt = self.run(alpha, flags)
-        assert int(self.layer.workspace[4:8].view(torch.int32).item()) == 0
+        assert workspace_ok(self.layer.workspace)
         ref = oracle.mlp_block(self.h, self.norm_w, self.eps, self.packed, self.wg, self.wu, self.wd, alpha)
         m_ref = ref["mask"]
+        # per-row h3 (h without W_up): x is rounded to fp16 on each side separately
+        X = oracle.fp16_to_f64(ref["x"])
+        check_h3(self.layer.workspace, self.k, self.d, X.shape[0], m_ref, ref["h3"] if self.wu is not None else
+                 ref["h"], X, fp16_rows(self.wg), None if self.wu is None else fp16_rows(self.wu), ref["g"],
+                 x_ulp=True)
         assert np.array_equal(mask.cpu().numpy(), m_ref)
         nref = int(m_ref.sum())
         assert int(n.item()) == nref

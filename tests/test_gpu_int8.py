@@ -18,6 +18,7 @@ import torch
 
 import oracle
 import paper_2411_12692_amd as si
+from h3check import check_h3, int8_rows, workspace_ok
 from paper_2411_12692_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -62,10 +63,6 @@ class I8Case:
         return oracle.int8_mlp(self.qg, self.sg, self.qu, self.su, self.qd, self.sd, self.x, mask)
 
 
-def workspace_errors(ws: torch.Tensor) -> int:
-    return int(ws[4:8].view(torch.int32).item())
-
-
 def check_weights(c: I8Case):
     L = c.layer
     assert np.array_equal(L.q_gate.cpu().numpy(), c.qg)
@@ -80,8 +77,13 @@ def check_weights(c: I8Case):
 
 
 def check(c: I8Case, mask_ref, y, cnt=None, flags=0):
-    assert workspace_errors(c.layer.workspace) == 0
+    """y, the counters and the per-row h3 of the call just made (the last one
+    on the layer's workspace) against the oracle."""
+    assert workspace_ok(c.layer.workspace)
     out = c.oracle_mlp(mask_ref)
+    X = oracle.fp16_to_f64(np.atleast_2d(c.x))
+    check_h3(c.layer.workspace, c.k, c.d, X.shape[0], mask_ref, out["h3"], X, int8_rows(c.qg, c.sg),
+             int8_rows(c.qu, c.su) if c.gated else None, out["g"])
     yr = out["y"]
     yg = y.cpu().numpy().astype(np.float64)
     nb = np.linalg.norm(yr)

@@ -15,6 +15,7 @@ import torch
 
 import oracle
 import paper_2411_12692_amd as si
+from h3check import check_h3, fp16_rows, workspace_ok
 from paper_2411_12692_amd import synth
 
 pytestmark = pytest.mark.gpu
@@ -88,9 +89,10 @@ def check_predict(c: Case, x, alpha):
 
 
 def device_errors(ws: torch.Tensor) -> int:
-    """Sticky device-side error bits the kernels keep in the workspace header
-    (a wait that hit its spin limit, an out-of-range row)."""
-    return int(ws[4:8].view(torch.int32).item())
+    """Status of the sticky device-side error word the kernels keep in the
+    workspace header (a wait that hit its spin limit, an out-of-range row),
+    through ``si_workspace_check``: 0 = SI_OK."""
+    return si.workspace_check(ws)
 
 
 def check_list(idx, n, mask_ref):
@@ -100,9 +102,15 @@ def check_list(idx, n, mask_ref):
     assert np.array_equal(idx.cpu().numpy()[:nref], oracle.active_rows(mask_ref))
 
 
-def check_mlp(c: Case, x, mask_ref, y, counters=None, flags=0):
+def check_mlp(c: Case, x, mask_ref, y, counters=None, flags=0, h3=True):
+    """y, the work counters and (``h3``: the MLP call with this mask was the
+    last call on the layer's workspace) the per-row h3 against the oracle."""
     assert device_errors(c.layer.workspace) == 0
     out = oracle.sparse_mlp(c.wg, c.wu, c.wd, x, mask_ref)
+    if h3:
+        X = oracle.fp16_to_f64(np.atleast_2d(x))
+        check_h3(c.layer.workspace, c.k, c.d, X.shape[0], mask_ref, out["h3"], X, fp16_rows(c.wg), fp16_rows(c.wu),
+                 out["g"])
     yr = out["y"]
     yg = y.cpu().numpy().astype(np.float64)
     err = rel_l2(yg, yr)
@@ -210,7 +218,7 @@ def test_separate_calls_match_fused(tiny):
     torch.cuda.synchronize()
     m_ref = oracle.predict_rows(tiny.packed, tiny.x, 1.0)[0]
     for y in (y1, y2, y3):
-        check_mlp(tiny, tiny.x, m_ref, y)
+        check_mlp(tiny, tiny.x, m_ref, y)  # h3: of the fused call, the last one (same rows as the others)
     assert torch.allclose(y1, y3, rtol=1e-5, atol=1e-6)
 
 
@@ -269,9 +277,9 @@ def test_batch_union(b):
     c = Case.planted(512, 1376, 0.9, config=1, b=b)
     x = to_dev(c.x)
     for alpha in [1.0, 1.45]:
+        m_ref = check_predict(c, c.x, alpha)
         y, (mask, idx, n, cnt) = c.layer(x, alpha, outputs=True)
         torch.cuda.synchronize()
-        m_ref = check_predict(c, c.x, alpha)
         assert np.array_equal(mask.cpu().numpy(), m_ref)
         check_list(idx, n, m_ref)
         check_mlp(c, c.x, m_ref, y, cnt)
@@ -285,9 +293,9 @@ def test_batch_7b_fused(b):
     the read counters may exceed the oracle's n_up and n_down but never
     n_gate."""
     c = Case.planted(4096, 11008, 0.9, config=2, b=b)
+    m_ref = check_predict(c, c.x, 1.0)
     y, (mask, idx, n, cnt) = c.layer(to_dev(c.x), 1.0, outputs=True)
     torch.cuda.synchronize()
-    m_ref = check_predict(c, c.x, 1.0)
     assert np.array_equal(mask.cpu().numpy(), m_ref)
     check_list(idx, n, m_ref)
     check_mlp(c, c.x, m_ref, y, cnt)
@@ -325,17 +333,18 @@ def test_batch_wide_rows(k, d, b):
     c = Case(rand_bits(rng, (k, d), False), rand_bits(rng, (k, d), False), rand_bits(rng, (d, k), False),
              rand_bits(rng, (b, d), False), max_batch=b)
     for alpha in [1.0, math.inf]:
+        m_ref = check_predict(c, c.x, alpha)
         y, (mask, idx, n, cnt) = c.layer(to_dev(c.x), alpha, outputs=True)
         torch.cuda.synchronize()
-        m_ref = check_predict(c, c.x, alpha)
         assert np.array_equal(mask.cpu().numpy(), m_ref)
         check_list(idx, n, m_ref)
         check_mlp(c, c.x, m_ref, y, cnt)
         # the list-driven and the mask-driven sparse MLP on the same rows
         y1, c1 = c.layer.sparse_mlp(to_dev(c.x), mask, idx, n, counters=True)
-        y2, c2 = c.layer.sparse_mlp(to_dev(c.x), mask=mask, counters=True)
         torch.cuda.synchronize()
         check_mlp(c, c.x, m_ref, y1, c1)
+        y2, c2 = c.layer.sparse_mlp(to_dev(c.x), mask=mask, counters=True)
+        torch.cuda.synchronize()
         check_mlp(c, c.x, m_ref, y2, c2)
 
 
@@ -365,12 +374,13 @@ def test_random_shapes_every_form(seed):
     m[int(rng.integers(0, k))] = True
     rows = np.flatnonzero(m).astype(np.int32)
     y1, c1 = c.layer.sparse_mlp(x, mask=torch.from_numpy(m.astype(np.uint8)).to(DEV), counters=True)
+    torch.cuda.synchronize()
+    check_mlp(c, c.x, m, y1, c1)
     lst = np.full(k, -1, dtype=np.int32)
     lst[: rows.size] = rows
     y2, c2 = c.layer.sparse_mlp(x, None, torch.from_numpy(lst).to(DEV),
                                 torch.tensor([rows.size], dtype=torch.int32, device=DEV), counters=True)
     torch.cuda.synchronize()
-    check_mlp(c, c.x, m, y1, c1)
     check_mlp(c, c.x, m, y2, c2)
 
 
@@ -404,9 +414,9 @@ def l7b():
 @pytest.mark.parametrize("alpha", [0.7, 1.0, 1.03, 1.45, 1.5])
 def test_7b_layer(l7b, alpha):
     x = to_dev(l7b.x)
+    m_ref = check_predict(l7b, l7b.x, alpha)
     y, (mask, idx, n, cnt) = l7b.layer(x, alpha, outputs=True)
     torch.cuda.synchronize()
-    m_ref = check_predict(l7b, l7b.x, alpha)
     assert np.array_equal(mask.cpu().numpy(), m_ref)
     check_list(idx, n, m_ref)
     check_mlp(l7b, l7b.x, m_ref, y, cnt)
@@ -415,9 +425,9 @@ def test_7b_layer(l7b, alpha):
 def test_13b_layer():
     c = Case.planted(5120, 13824, 0.88, config=4)
     x = to_dev(c.x)
+    m_ref = check_predict(c, c.x, 1.0)
     y, (mask, idx, n, cnt) = c.layer(x, 1.0, outputs=True)
     torch.cuda.synchronize()
-    m_ref = check_predict(c, c.x, 1.0)
     assert np.array_equal(mask.cpu().numpy(), m_ref)
     check_list(idx, n, m_ref)
     check_mlp(c, c.x, m_ref, y, cnt)
@@ -446,3 +456,37 @@ def test_first_call_on_a_fresh_workspace(flags):
     m_ref = oracle.predict_rows(c.packed, c.x, 1.0)[0]
     assert np.array_equal(mask.cpu().numpy(), m_ref)
     check_mlp(c, c.x, m_ref, y, cnt, flags=flags)
+
+
+@pytest.mark.parametrize("b", [1, 3])
+def test_multi_launch_gated_every_form(b):
+    """Above 256 rows per compute unit (k = 65600 at d = 128) every gated call
+    takes the multi-launch path: the predictor alone, the fused predict +
+    gate/up followed by the down-projection, and the mask and list forms of
+    the sparse MLP.  Masks, lists and counts bit-exact, y and the h3 of every
+    kept row against the oracle at alpha = 1 and +inf.  This path keeps h3 as
+    plain floats in the workspace, so the workspace is zero-filled before
+    each MLP call: no value of an earlier call can pass for this one's."""
+    k, d = 65600, 128
+    assert si._lib.load().si_single_launch(k, d, b) == 0
+    rng = np.random.default_rng(65600 + b)
+    c = Case(rand_bits(rng, (k, d), False), rand_bits(rng, (k, d), False), rand_bits(rng, (d, k), False),
+             rand_bits(rng, (b, d), False), max_batch=b)
+    x = to_dev(c.x)
+    for alpha in [1.0, math.inf]:
+        print(f"multi-launch k={k} d={d} b={b} alpha={alpha}", flush=True)
+        m_ref = check_predict(c, c.x, alpha)
+        c.layer.workspace.zero_()
+        y, (mask, idx, n, cnt) = c.layer(x, alpha, outputs=True)
+        torch.cuda.synchronize()
+        assert np.array_equal(mask.cpu().numpy(), m_ref)
+        check_list(idx, n, m_ref)
+        check_mlp(c, c.x, m_ref, y, cnt)
+        c.layer.workspace.zero_()
+        y1, c1 = c.layer.sparse_mlp(x, mask=mask, counters=True)
+        torch.cuda.synchronize()
+        check_mlp(c, c.x, m_ref, y1, c1)
+        c.layer.workspace.zero_()
+        y2, c2 = c.layer.sparse_mlp(x, mask, idx, n, counters=True)
+        torch.cuda.synchronize()
+        check_mlp(c, c.x, m_ref, y2, c2)

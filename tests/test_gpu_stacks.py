@@ -65,7 +65,7 @@ def test_stack_decode(cfg):
                                 y.cpu().numpy().astype(np.float64)))
     torch.cuda.synchronize()
     for lay in layers:
-        assert int(lay.workspace[4:8].view(torch.int32).item()) == 0
+        assert si.workspace_check(lay.workspace) == 0
     for l, t, x, mask, idx, n, y in records:
         wg, wu, wd = host[l]
         packed = oracle.pack_signs(wg)

@@ -64,6 +64,6 @@ def test_sweep(s):
         assert int(n.item()) == nref
         assert np.array_equal(idx.cpu().numpy()[:nref], oracle.active_rows(m_ref))
         check_y(yf, oracle.sparse_mlp(wg, wu, wd, xh, m_ref)["y"])
-    assert int(layer.workspace[4:8].view(torch.int32).item()) == 0
+    assert si.workspace_check(layer.workspace) == 0
     del layer, L
     torch.cuda.empty_cache()
