@@ -393,6 +393,10 @@ def report_alpha(args, si, synth, dev):
         pos = [schedule.gate_positive(p.w_gate, p.x) for p in pls]
         del pls
         ys = [torch.empty(1, D, dtype=torch.float32, device=dev) for _ in range(L)]
+        # the dense MLP through the same kernel: every row kept, every row of
+        # all three matrices read (alpha = +inf without actual sparsity)
+        dense = graph_us(lambda i: layers[i % L](xs[i % L], math.inf, flags=si.SI_NO_AS, y=ys[i % L]), 4 * L,
+                         reps=16)
         dense_torch = None
         if name == "planted":
             dense_torch = graph_us(lambda i: dense_torch_mlp(layers[i % L].w_gate, layers[i % L].w_up,
@@ -424,8 +428,8 @@ def report_alpha(args, si, synth, dev):
                              "missed_rows_total": sum(x["missed"] for x in q),
                              "sparse_precision": round(sum(x["sparse_precision"] for x in q) / L, 5),
                              "sparse_recall": round(sum(x["sparse_recall"] for x in q) / L, 5)})
-            dense = rows[-1]["us_per_layer"]
             for r in rows:
+                r["dense_call_us"] = round(dense, 3)
                 r["speedup_vs_dense_call"] = round(dense / r["us_per_layer"], 2)
                 if dense_torch is not None:
                     r["speedup_vs_torch_dense"] = round(dense_torch / r["us_per_layer"], 2)

@@ -72,10 +72,13 @@ typedef enum {
                        the work differs.  Used for the paper's +-AS ablation. */
 #define SI_NO_SPECULATION 2u /* read W_up / W_down^T rows strictly after the
                        values that decide whether they are needed.  By default
-                       the single-kernel path requests them early for rows
-                       whose count is far inside the Eq. (2) threshold
-                       (N_neg < T - d/16), which are almost surely active;
-                       results are identical, only the work may differ. */
+                       the single-kernel path requests them with the W_gate
+                       row for rows that are likely active: with one token,
+                       the rows Eq. (2) would keep at alpha = 1 (N_neg <=
+                       d/2; rows kept only because alpha > 1 wait for their
+                       gate value); with 2-4 tokens, rows d/16 inside that;
+                       with 5-8 tokens, every kept row.  Results are
+                       identical; only the work may differ. */
 
 /* Human-readable reason of the last non-SI_OK status on this thread. */
 const char* si_last_error(void);

@@ -12,11 +12,24 @@ namespace {
 
 thread_local char g_err[512] = "";
 
-// Rows with N_neg < T - margin count as surely kept: their W_up and W_down^T
-// requests go out before the gate result.  With 5-8 tokens the union of the
-// tokens' kept sets covers nearly every row, so every kept row is treated so
-// (margin 0): the few wasted W_up reads cost less than waiting for the gate.
-int confident_margin(int d, int b) { return b > 4 ? 0 : d / 16; }
+int32_t threshold(float alpha, int d);
+
+// Rows with N_neg < T - margin count as surely active: their W_up and
+// W_down^T requests go out with the W_gate row, before the gate result.
+// Products of the signs are symmetric (Section IV-A), so a row whose signs
+// agree with the token's on at least half of the elements (the rows Eq. (2)
+// keeps at alpha = 1: N_neg < T(1)) is more likely positive than not, and a
+// row kept only because alpha > 1 is more likely zero: those wait for their
+// gate value, so a larger alpha never adds speculative reads.  With 2-4
+// tokens the kept rows of one token are confident only d/16 below that (a
+// row kept by a fresh token sits near N_neg = d/2); with 5-8 tokens the union
+// of the tokens' kept sets is nearly every row and nearly every one is active
+// for some token, so every kept row is treated as confident.
+int confident_margin(int d, int b, int T) {
+  if (b > 4) return 0;
+  const int T1 = threshold(1.0f, d);
+  return (T > T1 ? T - T1 : 0) + (b == 1 ? 0 : d / 16);
+}
 
 si_status fail(si_status s, const char* fmt, ...) {
   va_list ap;
@@ -336,7 +349,7 @@ si_status predict_sparse_mlp_impl(const uint32_t* signs, const uint16_t* w_gate,
     c.d = d;
     c.b = b;
     c.T = T;
-    c.margin = confident_margin(d, b);
+    c.margin = confident_margin(d, b, c.T);
     c.flags = flags;
     c.mask = mask;
     c.idx = active_idx;
@@ -438,7 +451,7 @@ si_status si_rmsnorm_predict_sparse_mlp(const float* h, const float* norm_w, flo
   c.d = d;
   c.b = b;
   c.T = si_alpha_threshold(alpha, d);
-  c.margin = confident_margin(d, b);
+  c.margin = confident_margin(d, b, c.T);
   c.flags = flags;
   c.mask = mask;
   c.idx = active_idx;
@@ -515,7 +528,7 @@ si_status int8_impl(bool predict, const uint32_t* signs, const int8_t* w_gate, c
   c.b = b;
   if (predict) {
     c.T = si_alpha_threshold(alpha, d);
-    c.margin = confident_margin(d, b);
+    c.margin = confident_margin(d, b, c.T);
     c.mask = mask;
     c.idx = active_idx;
   }
