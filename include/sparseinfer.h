@@ -250,6 +250,29 @@ si_status si_predict_sparse_mlp(const uint32_t* signs, const uint16_t* w_gate, c
                                 int32_t* counters, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * si_predict_sparse_mlp without a workspace argument.  Its scratch is one
+ * array of 8 MiB per device inside the library (a file-scope device array,
+ * held on every device the library runs on until the process ends); the
+ * call allocates and frees nothing.  Arguments, outputs and errors as
+ * si_predict_sparse_mlp without workspace / workspace_bytes; shapes whose
+ * workspace (si_workspace_bytes(k, d, b)) exceeds 8 MiB return
+ * SI_ERR_WORKSPACE (every k <= 65536 fits, at any d and b).
+ * Every call on one device shares that device's array: calls that can
+ * overlap on one device (two streams, two host threads) race and must not
+ * be made.  Nothing needs clearing between calls: the array starts
+ * zero-filled, and a call reads only words it wrote itself or that carry its
+ * own call tag, whatever shapes earlier calls had.  After a bounded wait has
+ * given up (see "Co-residency") the later single-launch calls of this entry
+ * point on that device fill y with NaN until the process ends.
+ */
+si_status si_predict_sparse_mlp_noalloc(const uint32_t* signs, const uint16_t* w_gate, const uint16_t* w_up,
+                                        const uint16_t* w_down_t, int k, int d, const uint16_t* x, int b,
+                                        float alpha, uint8_t* mask, int32_t* active_idx, int32_t* n_active,
+                                        float* y, uint32_t flags, int32_t* counters, void* stream);
+
+/*
  * Non-gated ReLU MLP: the MLP block of models without step 2 of Section III
  * (no W_up; e.g. OPT and Falcon after ReLUfication):
  *   MLP(X) = ReLU(X W_fc1) W_down^T.

@@ -51,6 +51,7 @@ SIGNATURES = {
     "si_sparse_mlp": (_i, [_p, _p, _p, _i, _i, _p, _i, _p, _p, _p, _p, _p, _sz, _u32, _p, _p]),
     "si_predict_sparse_mlp": (_i, [_p, _p, _p, _p, _i, _i, _p, _i, _f, _p, _p, _p, _p, _p, _sz, _u32,
                                    _p, _p]),
+    "si_predict_sparse_mlp_noalloc": (_i, [_p, _p, _p, _p, _i, _i, _p, _i, _f, _p, _p, _p, _p, _u32, _p, _p]),
     "si_sparse_relu_mlp": (_i, [_p, _p, _i, _i, _p, _i, _p, _p, _p, _p, _p, _sz, _u32, _p, _p]),
     "si_predict_sparse_relu_mlp": (_i, [_p, _p, _p, _i, _i, _p, _i, _f, _p, _p, _p, _p, _p, _sz, _u32,
                                         _p, _p]),

@@ -1,4 +1,5 @@
 // C ABI of libsparseinfer: argument validation, Eq. (2) threshold, launches.
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdint>
@@ -596,3 +597,56 @@ si_status si_predict_sparse_mlp_i8(const uint32_t* signs, const int8_t* w_gate, 
 }
 
 }  // extern "C"
+
+// ---- the whole path without a caller's workspace ---------------------------
+
+namespace {
+
+// The scratch of si_predict_sparse_mlp_noalloc: one array per device, zero at
+// load (a zero-filled workspace is the state before a first call) and kept
+// from one call to the next exactly like a caller's workspace.
+constexpr size_t kScratchBytes = (size_t)8 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+// The device address of `scratch` on each device (its host-side name is not
+// a device address), looked up once per device with that device current.
+std::atomic<void*> g_scratch_ptr[si::kMaxDevices];
+
+si_status scratch_ptr(void** out) {
+  int dev = 0;
+  if (si_status s = hip_status(hipGetDevice(&dev), "hipGetDevice")) return s;
+  if (dev < 0 || dev >= si::kMaxDevices) return fail(SI_ERR_HIP, "device %d beyond the %d supported", dev, si::kMaxDevices);
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    if (si_status s = hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)"))
+      return s;
+    g_scratch_ptr[dev].store(p, std::memory_order_release);
+  }
+  *out = p;
+  return SI_OK;
+}
+
+}  // namespace
+
+extern "C" si_status si_predict_sparse_mlp_noalloc(const uint32_t* signs, const uint16_t* w_gate,
+                                                   const uint16_t* w_up, const uint16_t* w_down_t, int k, int d,
+                                                   const uint16_t* x, int b, float alpha, uint8_t* mask,
+                                                   int32_t* active_idx, int32_t* n_active, float* y, uint32_t flags,
+                                                   int32_t* counters, void* stream) {
+  REQUIRE_PTR(signs);
+  REQUIRE_PTR(w_gate);
+  REQUIRE_PTR(w_up);
+  REQUIRE_PTR(w_down_t);
+  REQUIRE_PTR(x);
+  REQUIRE_PTR(y);
+  if (si_status s = check_kd(k, d)) return s;
+  if (si_status s = check_b(b)) return s;
+  const size_t need = si::ws_layout(k, b).total;
+  if (need > kScratchBytes)
+    return fail(SI_ERR_WORKSPACE, "k=%d b=%d needs %zu bytes of scratch; the no-allocation call holds %zu per device",
+                k, b, need, kScratchBytes);
+  void* ws = nullptr;
+  if (si_status s = scratch_ptr(&ws)) return s;
+  return predict_sparse_mlp_impl(signs, w_gate, w_up, w_down_t, k, d, x, b, alpha, mask, active_idx, n_active, y,
+                                 ws, kScratchBytes, flags, counters, stream);
+}

@@ -170,3 +170,17 @@ def test_workspace_check_and_read_h3_validation(lib):
     for name, args, want in cases:
         st = _lib.status(name, *args)
         assert st == want, (name, args, st, _lib.last_error())
+
+
+def test_noalloc_validation(lib):
+    """The no-allocation entry point rejects shapes beyond its 8 MiB scratch
+    and missing pointers before touching the device."""
+    k, d, b = 1 << 20, 4096, 8
+    assert lib.si_workspace_bytes(k, d, b) > 8 << 20
+    args = (_p(A), _p(A), _p(A), _p(A), k, d, _p(A), b, 1.0, None, None, None, _p(A), 0, None, None)
+    assert _lib.status("si_predict_sparse_mlp_noalloc", *args) == _lib.SI_ERR_WORKSPACE
+    assert "scratch" in _lib.last_error()
+    args = (_p(A), _p(A), None, _p(A), 11008, 4096, _p(A), 1, 1.0, None, None, None, _p(A), 0, None, None)
+    assert _lib.status("si_predict_sparse_mlp_noalloc", *args) == _lib.SI_ERR_NULL
+    args = (_p(A), _p(A), _p(A), _p(A), 11008, 4096, _p(A), 9, 1.0, None, None, None, _p(A), 0, None, None)
+    assert _lib.status("si_predict_sparse_mlp_noalloc", *args) == _lib.SI_ERR_SHAPE
