@@ -226,12 +226,27 @@ def cpu_baseline(layers_host, alpha, budget_s, k=K, d=D, block=None, int8=False)
     }
 
 
+def upload_graph(graph, stream):
+    """hipGraphUpload of an instantiated graph (no kernel runs): a graph's
+    first replay would otherwise also pay for moving it to the device."""
+    import torch
+
+    hip = ctypes.CDLL("libamdhip64.so")
+    rc = hip.hipGraphUpload(ctypes.c_void_p(graph.raw_cuda_graph_exec()), ctypes.c_void_p(stream.cuda_stream))
+    if rc != 0:
+        raise RuntimeError(f"hipGraphUpload returned {rc}")
+    torch.cuda.synchronize()
+
+
 def time_steps(step, steps, warmup):
     """Exactly ``warmup`` untimed steps (launched one by one on the timing
     stream), then exactly ``steps`` timed steps replayed from one HIP graph of
     ``steps`` launches (step i runs layer i mod pool, continuing the
-    rotation).  Events on the replay stream bracket the one replay, with a
-    synchronization on both sides.  Returns (us per step, wall us per step)."""
+    rotation), uploaded to the device before the replay.  Events on the
+    replay stream bracket the one replay, with a synchronization on both
+    sides; the time includes the replay's own start (about 20 us per replay on
+    the MI355X, so short runs read slower).  Returns (us per step, wall us
+    per step)."""
     import torch
 
     stream = torch.cuda.Stream()
@@ -244,6 +259,7 @@ def time_steps(step, steps, warmup):
         for i in range(warmup, warmup + steps):
             step(i)
     torch.cuda.synchronize()
+    upload_graph(graph, stream)
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
