@@ -70,12 +70,22 @@ def algorithmic_bytes(k, d, b, n_gate, n_up, n_down, block=False, int8=False):
     return k * d // 8 + x_bytes + 2 * d * (n_gate + n_up + n_down) + 4 * d * b
 
 
-COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_7b_s0.9_counters.txt")
-RELU_COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_opt6.7b_relu_s0.9_counters.txt")
-INT8_COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_7b_int8_s0.9_counters.txt")
-BLOCK_COUNTERS_FILE = os.path.join(ROOT, "profiles", "k_owned_7b_block_s0.9_counters.txt")
 KERNEL_SOURCES = ("paper_2411_12692_amd/csrc/owned.hip", "paper_2411_12692_amd/csrc/layer_common.h",
                   "paper_2411_12692_amd/csrc/si_device.h")
+
+
+def workload_tag(args):
+    """Name of the workload's profile summaries under profiles/."""
+    if args.mlp == "relu":
+        return "k_owned_opt6.7b_relu_s0.9"
+    shape = "13b" if args.shape == "13b" else "7b"
+    form = {"int8": "_int8", "block": "_block"}.get(args.mlp, "")
+    s = 0.88 if args.shape == "13b" else 0.9
+    return f"k_owned_{shape}{form}" + (f"_b{args.batch}_union" if args.batch > 1 else "") + f"_s{s}"
+
+
+def counters_file(args):
+    return os.path.join(ROOT, "profiles", workload_tag(args) + "_counters.txt")
 
 
 def kernel_sources_sha256():
@@ -88,7 +98,7 @@ def kernel_sources_sha256():
     return h.hexdigest()
 
 
-def measured_traffic(counters_file=COUNTERS_FILE):
+def measured_traffic(counters_file):
     """HBM bytes per k_owned launch from the committed FETCH_SIZE/WRITE_SIZE
     summary, or None when that summary was taken on other kernel sources."""
     try:
@@ -116,6 +126,12 @@ def parse():
                     help="gated: the 7B-shaped gated MLP (default); relu: the non-gated ReLU MLP of an "
                          "OPT-6.7B-shaped layer; block: the 7B layer with RMSNorm and residual fused; int8: the "
                          "7B layer with INT8 weights")
+    ap.add_argument("--shape", choices=("7b", "13b"), default="7b",
+                    help="7b: the 7B-shaped layer (d=4096, k=11008, s=0.9; default); 13b: the 13B-shaped layer "
+                         "(d=5120, k=13824, s=0.88) of the 13B stack (gated, int8 and block forms)")
+    ap.add_argument("--batch", type=int, default=1,
+                    help="tokens per call: above 1, each step is the sparse MLP over the union of the tokens' planted "
+                         "active sets (the sparsity x batch workload, mask form); needs --no-cpu-baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU-oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-peak", action="store_true", help="skip the streaming-read probe")
@@ -723,18 +739,32 @@ def main():
     relu = args.mlp == "relu"
     block = args.mlp == "block"
     int8 = args.mlp == "int8"
-    D_, K_ = (RELU_D, RELU_K) if relu else (D, K)
+    B_ = args.batch
+    if not 1 <= B_ <= 8 or (B_ > 1 and (args.mlp != "gated" or not args.no_cpu_baseline)):
+        print("--batch takes 1..8 tokens, with --mlp gated and --no-cpu-baseline", file=sys.stderr)
+        sys.exit(2)
+    if relu and args.shape != "7b":
+        print("--mlp relu has its own (OPT-6.7B) shape", file=sys.stderr)
+        sys.exit(2)
+    big = args.shape == "13b"
+    D_, K_ = (RELU_D, RELU_K) if relu else (5120, 13824) if big else (D, K)
+    S_ = 0.88 if big else S
+    cfg = 7 if relu else 4 if big else 5 if B_ > 1 else 2
     EPS = 1e-5
     L = args.layers
-    layers, xs, hs, nws, host, host_block = [], [], [], [], [], []
+    layers, xs, hs, nws, host, host_block, umasks = [], [], [], [], [], [], []
     for l in range(L):
         # the non-gated layer takes the planted W_gate as its W_fc1
-        pl = synth.planted_layer(D_, K_, S, config=7 if relu else 2, layer=l, device=dev)
+        pl = synth.planted_layer(D_, K_, S_, config=cfg, layer=l, device=dev)
         if int8:  # quantized on the device, as at load
             layers.append(si.Int8MLPLayer(pl.w_gate, pl.w_up, pl.w_down))
         else:
-            layers.append(si.MLPLayer(pl.w_gate, None if relu else pl.w_up, pl.w_down))
-        xs.append(pl.x)
+            layers.append(si.MLPLayer(pl.w_gate, None if relu else pl.w_up, pl.w_down, max_batch=B_))
+        if B_ > 1:  # the batch's tokens and the union of their planted active sets
+            xs.append(synth.batch_tokens(pl, B_, config=cfg, layer_id=l))
+            umasks.append(synth.batch_union_mask(pl, B_, config=cfg, layer_id=l))
+        else:
+            xs.append(pl.x)
         if block:
             # residual stream with the planted token's signs, positive norm weight
             hs.append(pl.x.float() * 3.0)
@@ -758,12 +788,19 @@ def main():
     torch.cuda.synchronize()
     print(f"# pool of {L} layers ready", file=sys.stderr, flush=True)
 
-    ys = [torch.empty(1, D_, dtype=torch.float32, device=dev) for _ in range(L)]
+    ys = [torch.empty(B_, D_, dtype=torch.float32, device=dev) for _ in range(L)]
+    cnt_buf = torch.zeros(3, dtype=torch.int32, device=dev)
 
     def step(i, outputs=False):
         l = i % L
         if block:
             return layers[l].block(hs[l], nws[l], EPS, args.alpha, outputs=outputs, y=ys[l])
+        if B_ > 1:  # the mask form over the union mask (the caller's y)
+            lay = layers[l]
+            si._lib.call("si_sparse_mlp", si._vp(lay.w_gate), si._vp(lay.w_up), si._vp(lay.w_down_t), K_, D_,
+                         si._vp(xs[l]), B_, si._vp(umasks[l]), None, None, si._vp(ys[l]), si._vp(lay.workspace),
+                         lay.workspace.numel(), 0, si._vp(cnt_buf) if outputs else None, si._stream())
+            return (ys[l], (umasks[l], None, None, cnt_buf.clone())) if outputs else ys[l]
         return layers[l](xs[l], args.alpha, outputs=outputs, y=ys[l])
 
     # per layer (each layer's call is deterministic): the kept rows, the rows
@@ -791,9 +828,9 @@ def main():
     if args.profile_pass:
         profile_pass(step, L, max(args.launches, L), dev)
         return
-    bytes_per_layer = [algorithmic_bytes(K_, D_, 1, *c, block=block, int8=int8) for c in counts]
+    bytes_per_layer = [algorithmic_bytes(K_, D_, B_, *c, block=block, int8=int8) for c in counts]
     mean_bytes = sum(bytes_per_layer) / L
-    read_bytes = sum(algorithmic_bytes(K_, D_, 1, *c, block=block, int8=int8) for c in reads) / L
+    read_bytes = sum(algorithmic_bytes(K_, D_, B_, *c, block=block, int8=int8) for c in reads) / L
 
     steps, warmup = args.steps, args.warmup
     us_per_layer, wall_us = time_steps(step, steps, warmup)
@@ -826,8 +863,17 @@ def main():
     torch.cuda.synchronize()
     isolated_us = sum(a.elapsed_time(b) * 1e3 for a, b in evs) / M
 
+    shape_name = "13B" if big else "7B"
+    if relu:
+        metric = RELU_METRIC
+    elif B_ > 1:
+        metric = (f"µs per sparse MLP call with {B_} tokens (union of the tokens' planted active sets, mask form) "
+                  f"at {shape_name} shape, s={S_}; effective HBM GB/s")
+    else:
+        metric = (BLOCK_METRIC if block else INT8_METRIC if int8 else METRIC).replace(
+            "7B shape, s=0.9", f"{shape_name} shape, s={S_}")
     result = {
-        "metric": RELU_METRIC if relu else BLOCK_METRIC if block else INT8_METRIC if int8 else METRIC,
+        "metric": metric,
         "value": round(mean_bytes / us_per_layer / 1e3, 2),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -843,14 +889,15 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": (f"OPT-6.7B-shaped non-gated ReLU MLP layer (no W_up) d={D_} k={K_}" if relu else
-                         f"7B-shaped ReLU gated MLP layer d={D_} k={K_} as a decoder-block call (RMSNorm of the "
-                         f"fp32 residual stream, eps={EPS}, and the residual add fused)" if block else
-                         f"7B-shaped ReLU gated MLP layer d={D_} k={K_} with INT8 weights (symmetric, one float "
-                         f"scale per output channel, quantized on the device; fp16 x, fp32 accumulation)" if int8 else
-                         f"7B-shaped ReLU gated MLP layer d={D_} k={K_}") +
-                        f", planted sparsity s={S}, alpha={args.alpha}, batch 1, rotating pool of {L} layers, "
-                        f"HIP-graph replay",
-            "d": D_, "k": K_, "batch": 1, "alpha": args.alpha, "layers_in_pool": L,
+                         f"{shape_name}-shaped ReLU gated MLP layer d={D_} k={K_} as a decoder-block call (RMSNorm of "
+                         f"the fp32 residual stream, eps={EPS}, and the residual add fused)" if block else
+                         f"{shape_name}-shaped ReLU gated MLP layer d={D_} k={K_} with INT8 weights (symmetric, one "
+                         f"float scale per output channel, quantized on the device; fp16 x, fp32 accumulation)" if int8
+                         else f"{shape_name}-shaped ReLU gated MLP layer d={D_} k={K_}") +
+                        (f", planted sparsity s={S_}, alpha={args.alpha}, batch 1" if B_ == 1 else
+                         f", {B_} tokens, mask = union of {B_} per-token planted active sets of sparsity {S_}") +
+                        f", rotating pool of {L} layers, HIP-graph replay",
+            "d": D_, "k": K_, "batch": B_, "alpha": args.alpha if B_ == 1 else None, "layers_in_pool": L,
             "kept_rows": [c[0] for c in counts[:4]],
             "rows_needed": [c for c in counts[:2]],
             "rows_read": [c for c in reads[:2]],
@@ -864,8 +911,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(RELU_COUNTERS_FILE if relu else INT8_COUNTERS_FILE if int8 else
-                                        BLOCK_COUNTERS_FILE if block else COUNTERS_FILE),
+            "traffic": measured_traffic(counters_file(args)),
             "launch_us": round(us_per_layer, 3),
             "isolated_launch_us": round(isolated_us, 3),
         },
