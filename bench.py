@@ -671,8 +671,9 @@ def report_paths(args, si, synth, dev):
     pool of 8 layers), at planted s = 0.9 and 0.5 and 1, 2, 4, 8 tokens: the
     sparse MLP from the batch's union mask (the per-token planted sets, as
     in the sweep) and from the same rows as a list, the predictor alone, the
-    fused predict + MLP (which keeps the rows its own prediction gives), and
-    the dense call (every row kept)."""
+    fused predict + MLP (which keeps the rows its own prediction gives), the
+    dense call (every row kept) and the decoder-block call (RMSNorm and the
+    residual fused, on inputs whose normalised x is the plain call's)."""
     import torch
 
     L = 8
@@ -680,6 +681,7 @@ def report_paths(args, si, synth, dev):
         pls = [synth.planted_layer(D, K, s_, config=5, layer=l, device=dev) for l in range(L)]
         layers = [si.MLPLayer(p.w_gate, p.w_up, p.w_down, max_batch=8) for p in pls]
         ones = torch.ones(K, dtype=torch.uint8, device=dev)
+        nws = [torch.ones(D, device=dev) for _ in range(L)]
         for b in (1, 2, 4, 8):
             xs = [synth.batch_tokens(p, b, config=5, layer_id=l) for l, p in enumerate(pls)]
             ms = [synth.batch_union_mask(p, b, config=5, layer_id=l) for l, p in enumerate(pls)]
@@ -690,6 +692,9 @@ def report_paths(args, si, synth, dev):
                 idx[: nz.numel()] = nz
                 lists.append((idx, torch.tensor([nz.numel()], dtype=torch.int32, device=dev)))
             ys = [torch.empty(b, D, dtype=torch.float32, device=dev) for _ in range(L)]
+            # the decoder-block call on h = x * rms(x) with a unit norm weight: RMSNorm gives back
+            # x (to fp16 rounding), so the block call does the plain call's work plus the norm
+            hs = [x.float() * x.float().pow(2).mean(dim=1, keepdim=True).sqrt() for x in xs]
             fused_rows = 0
             for l in range(L):
                 _, (_, _, n, _) = layers[l](xs[l], 1.0, outputs=True)
@@ -704,6 +709,8 @@ def report_paths(args, si, synth, dev):
                 "predict_us": graph_us(lambda i: layers[i % L].predict(xs[i % L], 1.0), 4 * L, reps=8),
                 "fused_us": graph_us(lambda i: layers[i % L](xs[i % L], 1.0, y=ys[i % L]), 4 * L, reps=8),
                 "dense_us": graph_us(lambda i: layers[i % L].sparse_mlp(xs[i % L], mask=ones), 4 * L, reps=8),
+                "block_us": graph_us(lambda i: layers[i % L].block(hs[i % L], nws[i % L], 1e-5, 1.0, y=ys[i % L]),
+                                     4 * L, reps=8),
                 "workload": f"7B-shaped layer d={D} k={K}, planted s={s_}, {b} tokens, pool of {L}",
             }
             print(json.dumps({k: round(v, 3) if isinstance(v, float) else v for k, v in row.items()}), flush=True)

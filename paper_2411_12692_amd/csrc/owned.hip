@@ -87,6 +87,26 @@ constexpr int kODN = 8;            // W_down^T pieces per wave and down round
 constexpr int kODownRound = kOW * kODN;
 static_assert(kODN * kMaxB <= kWave, "a wave polls the h3 words of its pieces, one lane per (piece, token)");
 
+// The down-projection on the matrix cores (4-8 tokens, fp16 weights): the
+// group's rows in chunks of 32 (the K of one 16x16x32 fp16 MFMA), the tile's
+// 512 columns split over the 8 waves (64 each, four 16-column blocks), the
+// tokens padded to 16.  A chunk's W_down^T pieces pass through LDS, where
+// transposing reads give each lane 8 rows of one column (the A operand); h3
+// is the B operand, scaled per token and chunk by a power of two and split
+// into two fp16 parts (hi + lo), so the products keep fp32 precision for any
+// finite h3.
+constexpr int kMRows = 32;                // rows per chunk
+constexpr int kMInflight = 3;             // chunks whose pieces are in flight
+constexpr int kMPitch = kTile * 2 + 32;   // bytes per row of a chunk in LDS (padded against bank conflicts)
+constexpr int kMTok = 16;                 // tokens of the MFMA (b <= 8 used)
+static_assert(kMRows == 4 * kOW, "each wave stages 4 rows of a chunk (16 lanes per row)");
+static_assert(kTile == 4 * 16 * kOW, "four 16-column blocks per wave");
+template <int BM>
+struct MfmaLds {
+  unsigned char rows[kMRows * kMPitch];  // the chunk's pieces, row-major
+  uint16_t bop[2][kMTok][kMRows];        // h3 (hi, lo) as fp16, token-major
+};
+
 struct OwnedArgs {
   const u32x4* signs;
   const u32x4* wg;
@@ -124,6 +144,7 @@ struct OwnedLds {
   union {
     u32x4 xs[BM * kUnits];
     float dpart[kFold][BM][kTile];
+    unsigned char mf_raw[BM >= 4 ? sizeof(MfmaLds<BM>) : 16];  // the down-projection on the matrix cores
   };
   uint32_t xw[BM * kUnits / 4];  // sign words of the tokens
   // per-wave N_neg partial counts during the prediction; the group's kept
@@ -138,6 +159,8 @@ struct OwnedLds {
   float nsum[kOW][kMaxB];  // decoder-block mode: per-wave sums of squares of the tokens
   int n_own, n_up, n_down;
   uint32_t epoch, err;
+  uint32_t dmax[2][kMaxB];  // matrix-core down-projection: max |h3| bits per token (chunks alternate)
+  float dinv[kMaxB];        // and the inverse of its scale
 };
 
 template <int BM, int NU>
@@ -389,10 +412,11 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
   }
   // decoder-block mode with one token: the tile wave requests its 8 values
-  // of the residual h in the owner's tile now and stores them into y after
-  // the group exchange, so that neither the loads nor the stores delay the
-  // published masks (with more tokens the tile is copied before the first
-  // barrier)
+  // of the residual h in the owner's tile now (lane = unit of the tile) and
+  // stores them into y after the group exchange, so that neither the loads
+  // nor the stores delay the published masks (with more tokens the tile is
+  // copied while the finishing wave publishes: holding every token's values
+  // until after the exchange was no faster)
   float4 htile[2] = {};
   const int tunit = blk * kWave + lane;  // the lane's unit (8 columns) of the tile
   if constexpr (block_mode && BM == 1) {
@@ -417,8 +441,28 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   constexpr int J = (BM * XS + kXT - 1) / kXT;  // units per thread (incl. padding)
   constexpr bool kKeep = J <= 2;
   float4 hr[kKeep ? J : 1][2], wr[kKeep ? J : 1][2];
+  // otherwise (several tokens, or a wide row) thread tid takes the units
+  // u = tid + j kOT of every token: the unit of norm_w is read once for all
+  // tokens, and the b + 1 requests of a unit go out together.  Where they
+  // fit, the values stay in registers from the sums of squares to the
+  // scaling (which then runs right after the first barrier)
+  constexpr int JU = (XS + kOT - 1) / kOT;
+  constexpr bool kHold = JU * (BM + 1) * 8 <= 80;
+  float4 hk[kHold ? JU : 1][BM][2], wk[kHold ? JU : 1][2];
+  auto load_unit = [&](int u, float4 (&hv)[BM][2], float4 (&nv)[2]) {
+    const int uc = min(u, U - 1);
+    nv[0] = wg4[2 * uc];
+    nv[1] = wg4[2 * uc + 1];
+#pragma unroll
+    for (int t = 0; t < BM; ++t) {
+      const int i = min(t, b - 1) * U + uc;
+      hv[t][0] = hg[2 * i];
+      hv[t][1] = hg[2 * i + 1];
+    }
+  };
   // decoder-block mode: x = the fp16 rounding of h * r_t * norm_w, r_t the
-  // token's RMS normaliser from the block's sums of squares
+  // token's RMS normaliser from the block's sums of squares (the units kept
+  // in hr / wr)
   auto scale_x = [&]() {
     if (tid >= kXT) return;
     float r[BM];
@@ -430,7 +474,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       r[t] = 1.0f / sqrtf(v / (float)d + a.eps);
     }
 #pragma unroll
-    for (int j = 0; j < J; ++j) {
+    for (int j = 0; j < (kKeep ? J : 0); ++j) {
       const int i = tid + j * kXT, t = i / XS, u = i - t * XS;
       if (i < BM * XS) {
         u32x4 xv{0, 0, 0, 0};
@@ -438,24 +482,54 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
           float rt = 0.f;
 #pragma unroll
           for (int tt = 0; tt < BM; ++tt) rt = tt == t ? r[tt] : rt;
-          float4 p, q, wp, wq;
-          if constexpr (kKeep) {
-            p = hr[j][0];
-            q = hr[j][1];
-            wp = wr[j][0];
-            wq = wr[j][1];
-          } else {
-            p = hg[2 * (t * U + u)];
-            q = hg[2 * (t * U + u) + 1];
-            wp = wg4[2 * u];
-            wq = wg4[2 * u + 1];
-          }
+          const float4 p = hr[j][0], q = hr[j][1], wp = wr[j][0], wq = wr[j][1];
           xv.x = pack_h2((p.x * rt) * wp.x, (p.y * rt) * wp.y);
           xv.y = pack_h2((p.z * rt) * wp.z, (p.w * rt) * wp.w);
           xv.z = pack_h2((q.x * rt) * wq.x, (q.y * rt) * wq.y);
           xv.w = pack_h2((q.z * rt) * wq.z, (q.w * rt) * wq.w);
         }
         L.xs[i] = xv;
+      }
+    }
+  };
+  auto scale_units = [&]() {
+    float r[BM];
+#pragma unroll
+    for (int t = 0; t < BM; ++t) {
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < kOW; ++w) v += L.nsum[w][t];
+      r[t] = 1.0f / sqrtf(v / (float)d + a.eps);
+    }
+#pragma unroll
+    for (int j = 0; j < JU; ++j) {
+      const int u = tid + j * kOT;
+      if (u < XS) {
+        float4 hv[BM][2], nv[2];
+        if constexpr (kHold) {
+#pragma unroll
+          for (int t = 0; t < BM; ++t) {
+            hv[t][0] = hk[j][t][0];
+            hv[t][1] = hk[j][t][1];
+          }
+          nv[0] = wk[j][0];
+          nv[1] = wk[j][1];
+        } else {
+          load_unit(u, hv, nv);
+        }
+#pragma unroll
+        for (int t = 0; t < BM; ++t) {
+          u32x4 xv{0, 0, 0, 0};
+          if (t < b && u < U) {
+            const float4 p = hv[t][0], q = hv[t][1], wp = nv[0], wq = nv[1];
+            const float rt = r[t];
+            xv.x = pack_h2((p.x * rt) * wp.x, (p.y * rt) * wp.y);
+            xv.y = pack_h2((p.z * rt) * wp.z, (p.w * rt) * wp.w);
+            xv.z = pack_h2((q.x * rt) * wq.x, (q.y * rt) * wq.y);
+            xv.w = pack_h2((q.z * rt) * wq.z, (q.w * rt) * wq.w);
+          }
+          L.xs[t * XS + u] = xv;
+        }
       }
     }
   };
@@ -500,12 +574,50 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     // the fp32 residual stream: the sums of squares over the block, then
     // every unit of 8 values scaled and rounded.  Where a thread has at most
     // two units (b * d <= 8192) its h and norm_w values stay in registers
-    // between the two steps; otherwise they are read again.
+    // between the two steps; otherwise the units go one per thread and
+    // token column (above).
     float ss[BM];
 #pragma unroll
     for (int t = 0; t < BM; ++t) ss[t] = 0.f;
+    // the sign byte of x's unit: the XOR of the signs of h and norm_w (the
+    // scale is positive, and rounding to fp16 keeps the sign, zeros
+    // included), so the predictor's sign words need no norm
+    auto sign_byte = [](float4 p, float4 q) -> uint32_t {
+      return (__float_as_uint(p.x) >> 31) | ((__float_as_uint(p.y) >> 31) << 1) |
+             ((__float_as_uint(p.z) >> 31) << 2) | ((__float_as_uint(p.w) >> 31) << 3) |
+             ((__float_as_uint(q.x) >> 31) << 4) | ((__float_as_uint(q.y) >> 31) << 5) |
+             ((__float_as_uint(q.z) >> 31) << 6) | ((__float_as_uint(q.w) >> 31) << 7);
+    };
+    if constexpr (!kKeep) {
 #pragma unroll
-    for (int j = 0; j < J; ++j) {
+      for (int j = 0; j < JU; ++j) {
+        const int u = tid + j * kOT;
+        float4 hv[BM][2], nv[2];
+        load_unit(u, hv, nv);
+        if (u < U) {
+          const uint32_t wb = sign_byte(nv[0], nv[1]);
+#pragma unroll
+          for (int t = 0; t < BM; ++t) {
+            if (t < b) {
+              const float4 p = hv[t][0], q = hv[t][1];
+              ss[t] += p.x * p.x + p.y * p.y + p.z * p.z + p.w * p.w + q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
+              reinterpret_cast<uint8_t*>(L.xw)[t * 4 * W + u] = (uint8_t)(sign_byte(p, q) ^ wb);
+            }
+          }
+        }
+        if constexpr (kHold) {
+#pragma unroll
+          for (int t = 0; t < BM; ++t) {
+            hk[j][t][0] = hv[t][0];
+            hk[j][t][1] = hv[t][1];
+          }
+          wk[j][0] = nv[0];
+          wk[j][1] = nv[1];
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < (kKeep ? J : 0); ++j) {
       const int i = tid + j * kXT, t = i / XS, u = i - t * XS;
       if (tid < kXT && i < BM * XS && t < b && u < U) {
         const float4 p = hg[2 * (t * U + u)], q = hg[2 * (t * U + u) + 1];
@@ -516,24 +628,14 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         const float v = p.x * p.x + p.y * p.y + p.z * p.z + p.w * p.w + q.x * q.x + q.y * q.y + q.z * q.z + q.w * q.w;
 #pragma unroll
         for (int tt = 0; tt < BM; ++tt) ss[tt] += tt == t ? v : 0.f;
-        // the signs of this unit of x need no norm: each is the XOR of the
-        // signs of h and norm_w (the scale is positive, and rounding to
-        // fp16 keeps the sign, zeros included), so the predictor's sign
-        // byte is written now (byte u of the token's sign words)
+        // the predictor's sign byte of this unit (byte u of the token's
+        // sign words)
         const float4 wp = wg4[2 * u], wq = wg4[2 * u + 1];
         if constexpr (kKeep) {
           wr[j][0] = wp;
           wr[j][1] = wq;
         }
-        const uint32_t hb = (__float_as_uint(p.x) >> 31) | ((__float_as_uint(p.y) >> 31) << 1) |
-                            ((__float_as_uint(p.z) >> 31) << 2) | ((__float_as_uint(p.w) >> 31) << 3) |
-                            ((__float_as_uint(q.x) >> 31) << 4) | ((__float_as_uint(q.y) >> 31) << 5) |
-                            ((__float_as_uint(q.z) >> 31) << 6) | ((__float_as_uint(q.w) >> 31) << 7);
-        const uint32_t wb = (__float_as_uint(wp.x) >> 31) | ((__float_as_uint(wp.y) >> 31) << 1) |
-                            ((__float_as_uint(wp.z) >> 31) << 2) | ((__float_as_uint(wp.w) >> 31) << 3) |
-                            ((__float_as_uint(wq.x) >> 31) << 4) | ((__float_as_uint(wq.y) >> 31) << 5) |
-                            ((__float_as_uint(wq.z) >> 31) << 6) | ((__float_as_uint(wq.w) >> 31) << 7);
-        reinterpret_cast<uint8_t*>(L.xw)[t * 4 * W + u] = (uint8_t)(hb ^ wb);
+        reinterpret_cast<uint8_t*>(L.xw)[t * 4 * W + u] = (uint8_t)(sign_byte(p, q) ^ sign_byte(wp, wq));
       }
     }
     if (tid == 0) {
@@ -556,7 +658,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     if (owns_tile && wv == kTileWave) poison_tile(a.y, b, d, blk, lane);
     return;
   }
-  if constexpr (block_mode && !kKeep) scale_x();  // h and norm_w read again: before the counts, not behind the publishing stores
+  if constexpr (block_mode && !kKeep) scale_units();  // before the counts, not behind the publishing stores
   const uint32_t epoch = uniform(L.epoch);
   const uint32_t tag = epoch_tag(epoch);
   // consumed here, where the wait for it is covered by the token requests (a
@@ -648,14 +750,26 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     if (predict && any_rows && s + 1 < nsub) __syncthreads();  // the partial counts are reused
   }
   // decoder-block mode with several tokens: the owner's tile of y starts as
-  // the residual h (while the finishing wave publishes)
+  // the residual h (lane = unit of the tile; every token's unit is requested
+  // before any is stored)
   if constexpr (block_mode && BM > 1) {
-    if (owns_tile && wv == kTileWave) {
-      const int half_cols = min(kTile, d - blk * kTile) / 2;
-      for (int t = 0; t < b; ++t) {
-        const uint64_t* ht = reinterpret_cast<const uint64_t*>(a.h + (size_t)t * d + blk * kTile);
-        uint64_t* yt = reinterpret_cast<uint64_t*>(a.y + (size_t)t * d + blk * kTile);
-        for (int c = lane; c < half_cols; c += kWave) st_agent64(yt + c, ht[c]);
+    if (owns_tile && wv == kTileWave && tunit < U) {
+      float4 hv[BM][2];
+#pragma unroll
+      for (int t = 0; t < BM; ++t) {
+        const size_t i = (size_t)min(t, b - 1) * U + tunit;
+        hv[t][0] = hg[2 * i];
+        hv[t][1] = hg[2 * i + 1];
+      }
+#pragma unroll
+      for (int t = 0; t < BM; ++t) {
+        if (t < b) {
+          uint64_t* yu = reinterpret_cast<uint64_t*>(a.y + (size_t)t * d) + 4 * (size_t)tunit;
+          st_agent64(yu, ((uint64_t)__float_as_uint(hv[t][0].y) << 32) | __float_as_uint(hv[t][0].x));
+          st_agent64(yu + 1, ((uint64_t)__float_as_uint(hv[t][0].w) << 32) | __float_as_uint(hv[t][0].z));
+          st_agent64(yu + 2, ((uint64_t)__float_as_uint(hv[t][1].y) << 32) | __float_as_uint(hv[t][1].x));
+          st_agent64(yu + 3, ((uint64_t)__float_as_uint(hv[t][1].w) << 32) | __float_as_uint(hv[t][1].z));
+        }
       }
     }
   }
@@ -667,6 +781,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   if constexpr (block_mode && kKeep) scale_x();
 
   bool census_done = false;
+  if (tid < 2 * kMaxB) L.dmax[tid / kMaxB][tid % kMaxB] = 0u;
   if (a.mlp) {
     // ---- the block's group: the T blocks [g T, g T + T) (T = tiles of y);
     // member m takes an even share of the group's kept rows for gate/up and
@@ -860,7 +975,125 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     // row's pieces are requested (with several tokens a kept row almost
     // always has a non-zero h3; without speculation the rounds below run)
     bool pipelined = false;
-    if constexpr (BM >= 2) {
+    constexpr bool kMfma = BM >= 4 && !kI8;
+    bool mdone = false;      // the down item ran on the matrix cores (its tile is in macc)
+    float macc[4][4] = {};   // column block cb of the wave, D[4 g + i][token]: column 64 wv + 16 cb + 4 g + i
+    if constexpr (kMfma) {
+      if (spec_ok && dN > 0) {
+        pipelined = true;
+        mdone = true;
+        MfmaLds<BM>& M = *reinterpret_cast<MfmaLds<BM>*>(L.mf_raw);
+        const int nch = (dN + kMRows - 1) / kMRows;
+        // pieces: the thread stages row 4 wv + lane / 16 of each chunk, its
+        // 16-byte units lane % 16 + 16 j (j < 4) of the tile
+        const int prow = 4 * wv + (lane >> 4), pslot = lane & 15;
+        // h3 words: thread (row tid / BM, token tid % BM) for tid < 32 BM
+        // (whole waves); the last wave reads the tile's zero flag with the
+        // first chunk
+        const int hrow = tid / BM, htok = tid - (tid / BM) * BM;
+        const bool hwave = uniform(wv) < kMRows * BM / kWave;
+        const bool zwave = uniform(wv) == kOW - 1;
+        static_assert(kMRows * kMaxB / kWave < kOW, "the zero-flag wave reads no h3 words");
+        const int tcu = tile * kWave;  // the tile's first 16-byte unit of a row
+        auto request = [&](int c, u32x4(&pc)[4], uint64_t& w) {
+          const int q = min(c * kMRows + prow, dN - 1);
+          const u32x4* src = a.wdt + (size_t)(L.dent[q] & 0x7fffffffu) * U;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) pc[j] = load_nt(src + min(tcu + pslot + 16 * j, U - 1));
+          // the first read of the chunk's h3 words goes out right behind its
+          // pieces (a poll issued later would wait for every request before it)
+          if (hwave) {
+            const int hq = min(c * kMRows + hrow, dN - 1);
+            w = ld_agent64(a.h3e + (size_t)(L.dent[hq] & 0x7fffffffu) * b + min(htok, b - 1));
+          } else if (zwave && c == 0) {
+            w = ld_agent64(&a.zflag[tile]);
+          }
+        };
+        auto chunk = [&](int c, u32x4(&pc)[4], uint64_t& w) {
+          float v = 0.f;
+          if (hwave) {
+            const int hq = c * kMRows + hrow;
+            const bool ok = htok < b && hq < dN;
+            uint32_t payload = (uint32_t)w;
+            if (ok && (uint32_t)(w >> 32) != tag) {  // not published at the first read
+              const uint64_t* src[1] = {a.h3e + (size_t)(L.dent[hq] & 0x7fffffffu) * b + htok};
+              uint32_t o[1];
+              poll_words<1>(src, 1, tag, a.hdr, o);
+              payload = o[0];
+            }
+            v = ok ? __uint_as_float(payload) : 0.f;
+            if (ok) atomicMax(&L.dmax[c & 1][htok], __float_as_uint(v) & 0x7fffffffu);
+          } else if (zwave && c == 0) {
+            zok = (uint32_t)(w >> 32) == tag && (uint32_t)w == 1u;
+          }
+          if (c == 0) SI_TRACE_WAVE(3);
+          __syncthreads();  // (the first: every wave is past its gate/up, so x's LDS is free)
+          unsigned char* rb = M.rows + prow * kMPitch;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) *reinterpret_cast<u32x4*>(rb + (pslot + 16 * j) * 16) = pc[j];
+          if (hwave) {
+            // scale 2^(se - 127): the token's largest |h3| of the chunk
+            // lands in [2^14, 2^15), within fp16's range
+            const int e8 = (int)(L.dmax[c & 1][htok] >> 23);
+            const int se = min(268 - e8, 253);
+            const float vs = v * __uint_as_float((uint32_t)se << 23);
+            const _Float16 hi = (_Float16)vs;
+            const _Float16 lo = (_Float16)(vs - (float)hi);
+            M.bop[0][htok][hrow] = __builtin_bit_cast(uint16_t, hi);
+            M.bop[1][htok][hrow] = __builtin_bit_cast(uint16_t, lo);
+            if (hrow == 0) L.dinv[htok] = __uint_as_float((uint32_t)(254 - se) << 23);
+          }
+          if (tid < kMaxB) L.dmax[(c + 1) & 1][tid] = 0u;
+          if (c == 0)  // tokens BM..15 of the B operand stay zero
+            for (int i = tid; i < 2 * (kMTok - BM) * kMRows; i += kOT) {
+              const int hlf = i / ((kMTok - BM) * kMRows), r = i - hlf * ((kMTok - BM) * kMRows);
+              M.bop[hlf][BM + r / kMRows][r % kMRows] = 0;
+            }
+          if (c + kMInflight < nch) request(c + kMInflight, pc, w);
+          __syncthreads();
+          // lane (g = lane / 16, j16 = lane % 16): B = token j16's rows
+          // 8 g .. 8 g + 7; A = those rows of column j16 of the block, from
+          // two transposing reads (the 16 lanes of a group point at 4 rows x
+          // 4 column quads; lane 4 p + q receives column 4 p + q of each row)
+          const int g = lane >> 4, j16 = lane & 15;
+          typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+          typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+          typedef float f4 __attribute__((ext_vector_type(4)));
+          typedef short s4 __attribute__((ext_vector_type(4)));
+          typedef __attribute__((address_space(3))) s4 lds_s4;
+          const h8 bh = *reinterpret_cast<const h8*>(&M.bop[0][j16][8 * g]);
+          const h8 bl = *reinterpret_cast<const h8*>(&M.bop[1][j16][8 * g]);
+          const float inv = j16 < BM ? L.dinv[j16] : 0.f;
+          const unsigned char* ab = M.rows + (8 * g + (j16 >> 2)) * kMPitch + (64 * wv + 4 * (j16 & 3)) * 2;
+#pragma unroll
+          for (int cb = 0; cb < 4; ++cb) {
+            const h4 a0 = __builtin_bit_cast(h4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(ab + 32 * cb)));
+            const h4 a1 =
+                __builtin_bit_cast(h4, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(ab + 32 * cb + 4 * kMPitch)));
+            const h8 av = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+            f4 dv = {0.f, 0.f, 0.f, 0.f};
+            dv = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bh, dv, 0, 0, 0);
+            dv = __builtin_amdgcn_mfma_f32_16x16x32_f16(av, bl, dv, 0, 0, 0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) macc[cb][i] = fmaf(dv[i], inv, macc[cb][i]);
+          }
+          if (c == 0) SI_TRACE_WAVE(4);
+        };
+        u32x4 p0[4], p1[4], p2[4];
+        uint64_t w0 = 0, w1 = 0, w2 = 0;
+        static_assert(kMInflight == 3, "three chunks in flight");
+        request(0, p0, w0);
+        if (1 < nch) request(1, p1, w1);
+        if (2 < nch) request(2, p2, w2);
+        for (int c = 0; c < nch; c += kMInflight) {
+          chunk(c, p0, w0);
+          if (c + 1 < nch) chunk(c + 1, p1, w1);
+          if (c + 2 < nch) chunk(c + 2, p2, w2);
+        }
+        n_down = wv == 0 ? dN : 0;
+      }
+    }
+    if constexpr (BM >= 2 && !kMfma) {
       if (spec_ok && dN > 0) {
         pipelined = true;
         const int dcu = min(dunit, U - 1);  // column unit of the loads (in the row even past d)
@@ -966,13 +1199,26 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       }
     }
     if (lane == 0 && tile == 0 && n_down) atomicAdd(&L.n_down, n_down);
-    if (wv == 0 && lane == 0) L.wsum[0] = zok ? 1 : 0;
+    if (wv == (mdone ? kOW - 1 : 0) && lane == 0) L.wsum[0] = zok ? 1 : 0;
     // per-wave partial tiles folded in LDS (plain stores; x is no longer
     // needed): kFold waves store, the others add in turn
     constexpr int kFold = OwnedLds<BM, NU>::kFold;
     __syncthreads();
     const bool zok_all = L.wsum[0] != 0;
-    if (dN > 0) {
+    if (mdone) {
+      // every wave is past its chunks: its columns of the tile go to LDS in
+      // the fold's layout (token, column), so that the atomics below run
+      // over consecutive columns (in the MFMA's layout one atomic
+      // instruction would touch about 32 lines of y)
+      const int n = lane & 15;
+      if (n < BM) {
+#pragma unroll
+        for (int cb = 0; cb < 4; ++cb)
+          *reinterpret_cast<float4*>(&L.dpart[0][n][64 * wv + 16 * cb + 4 * (lane >> 4)]) =
+              float4{macc[cb][0], macc[cb][1], macc[cb][2], macc[cb][3]};
+      }
+    }
+    if (dN > 0 && !mdone) {
 #pragma unroll
       for (int pass = 0; pass < kOW / kFold; ++pass) {
         if (wv / kFold == pass) {
@@ -1008,7 +1254,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         const int t = i / kTile, c = i - t * kTile, col = tile * kTile + c;
         float v = 0.f;
 #pragma unroll
-        for (int s2 = 0; s2 < kFold; ++s2) v += L.dpart[s2][t][c];
+        for (int s2 = 0; s2 < kFold; ++s2) v += (mdone && s2 > 0) ? 0.f : L.dpart[s2][t][c];
         if constexpr (kI8) {
           if (col < d && v != 0.f) unsafeAtomicAdd(&a.y[(size_t)t * d + col], v * a.sd[col]);
         } else {
