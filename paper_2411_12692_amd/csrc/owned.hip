@@ -158,6 +158,7 @@ struct OwnedLds {
   int wsum[kOW];
   float nsum[kOW][kMaxB];  // decoder-block mode: per-wave sums of squares of the tokens
   int n_own, n_up, n_down;
+  int gpos;  // next gate/up position of the member's range not yet taken by a wave
   uint32_t epoch, err;
   uint32_t dmax[2][kMaxB];  // matrix-core down-projection: max |h3| bits per token (chunks alternate)
   float dinv[kMaxB];        // and the inverse of its scale
@@ -849,16 +850,17 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
     const int lo = (n * m) / T, hi = (n * (m + 1)) / T;  // this member's gate/up positions
     const int dN = n;                                     // the down item's positions
+    if (tid == 0) L.gpos = lo + kOW;
     __syncthreads();
     SI_TRACE_MARK(4);
 
-    // ---- 2. gate/up: wave w takes positions lo + w, lo + w + 8, ... and
-    // for each its W_gate row and (for confident rows, or without actual
+    // ---- 2. gate/up: wave w takes position lo + w, then the next position
+    // no wave has taken yet, and for each its W_gate row and (for confident rows, or without actual
     // sparsity) its W_up row at once; other rows read W_up only where some
     // token's ReLU output is positive.  Each wave works through its rows on
     // its own (no block barrier) and publishes h3 per row and token.
     int n_up = 0;
-    for (int pos = lo + wv; pos < hi; pos += kOW) {
+    for (int pos = lo + wv; pos < hi;) {
       const uint32_t e = L.dent[pos];
       const uint32_t row = e & 0x7fffffffu;
       float g[BM], u[BM];
@@ -946,6 +948,12 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
 #pragma unroll
       for (int t = 0; t < BM; ++t) hv = lane == t ? fmaxf(g[t], 0.f) * u[t] : hv;
       if (lane < b) st_agent64(&a.h3e[(size_t)row * b + lane], tagged(tag, __float_as_uint(hv)));
+      // the next free position of the member's range: the waves that the
+      // CU serves first take more rows (with a fixed stride the second wave
+      // of each SIMD finished its rows up to 10 us after the first)
+      int nxt = 0;
+      if (lane == 0) nxt = atomicAdd(&L.gpos, 1);
+      pos = __builtin_amdgcn_readfirstlane(nxt);
     }
     SI_TRACE_WAVE(1);
     if (lane == 0 && n_up) atomicAdd(&L.n_up, n_up);
