@@ -87,8 +87,9 @@ constexpr int kODN = 8;            // W_down^T pieces per wave and down round
 constexpr int kODownRound = kOW * kODN;
 static_assert(kODN * kMaxB <= kWave, "a wave polls the h3 words of its pieces, one lane per (piece, token)");
 
-// The down-projection on the matrix cores (4-8 tokens, fp16 weights): the
-// group's rows in chunks of 32 (the K of one 16x16x32 fp16 MFMA), the tile's
+// The down-projection on the matrix cores (4-8 tokens; INT8 pieces are
+// turned into fp16, exactly, on their way into LDS): the group's rows in
+// chunks of 32 (the K of one 16x16x32 fp16 MFMA), the tile's
 // 512 columns split over the 8 waves (64 each, four 16-column blocks), the
 // tokens padded to 16.  A chunk's W_down^T pieces pass through LDS, where
 // transposing reads give each lane 8 rows of one column (the A operand); h3
@@ -327,6 +328,8 @@ struct DownPiece {
     f[0] = (float)p0.x; f[1] = (float)p0.y; f[2] = (float)p1.x; f[3] = (float)p1.y;
     f[4] = (float)p2.x; f[5] = (float)p2.y; f[6] = (float)p3.x; f[7] = (float)p3.y;
   }
+  // the 8 columns as fp16 (the matrix-core down-projection's A operand)
+  static __device__ inline u32x4 as_f16(type v) { return v; }
 };
 template <>
 struct DownPiece<true> {
@@ -340,6 +343,18 @@ struct DownPiece<true> {
       f[i] = (float)(int8_t)(v.x >> (8 * i));
       f[4 + i] = (float)(int8_t)(v.y >> (8 * i));
     }
+  }
+  // the 8 INT8 values as fp16 (exact: |q| <= 128 < 2048), the column scales
+  // being applied at the tile's add into y
+  static __device__ inline u32x4 as_f16(type v) {
+    float f[8];
+    values(v, f);
+    u32x4 r;
+    r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(f[0], f[1]));
+    r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(f[2], f[3]));
+    r.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(f[4], f[5]));
+    r.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(f[6], f[7]));
+    return r;
   }
 };
 
@@ -983,7 +998,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     // row's pieces are requested (with several tokens a kept row almost
     // always has a non-zero h3; without speculation the rounds below run)
     bool pipelined = false;
-    constexpr bool kMfma = BM >= 4 && !kI8;
+    constexpr bool kMfma = BM >= 4;
     bool mdone = false;      // the down item ran on the matrix cores (its tile is in macc)
     float macc[4][4] = {};   // column block cb of the wave, D[4 g + i][token]: column 64 wv + 16 cb + 4 g + i
     if constexpr (kMfma) {
@@ -1003,11 +1018,12 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         const bool zwave = uniform(wv) == kOW - 1;
         static_assert(kMRows * kMaxB / kWave < kOW, "the zero-flag wave reads no h3 words");
         const int tcu = tile * kWave;  // the tile's first 16-byte unit of a row
-        auto request = [&](int c, u32x4(&pc)[4], uint64_t& w) {
+        typedef typename DP::type PT;
+        auto request = [&](int c, PT(&pc)[4], uint64_t& w) {
           const int q = min(c * kMRows + prow, dN - 1);
-          const u32x4* src = a.wdt + (size_t)(L.dent[q] & 0x7fffffffu) * U;
+          const size_t row = L.dent[q] & 0x7fffffffu;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) pc[j] = load_nt(src + min(tcu + pslot + 16 * j, U - 1));
+          for (int j = 0; j < 4; ++j) pc[j] = DP::load(a.wdt, row, U, min(tcu + pslot + 16 * j, U - 1));
           // the first read of the chunk's h3 words goes out right behind its
           // pieces (a poll issued later would wait for every request before it)
           if (hwave) {
@@ -1017,7 +1033,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
             w = ld_agent64(&a.zflag[tile]);
           }
         };
-        auto chunk = [&](int c, u32x4(&pc)[4], uint64_t& w) {
+        auto chunk = [&](int c, PT(&pc)[4], uint64_t& w) {
           float v = 0.f;
           if (hwave) {
             const int hq = c * kMRows + hrow;
@@ -1038,7 +1054,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
           __syncthreads();  // (the first: every wave is past its gate/up, so x's LDS is free)
           unsigned char* rb = M.rows + prow * kMPitch;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) *reinterpret_cast<u32x4*>(rb + (pslot + 16 * j) * 16) = pc[j];
+          for (int j = 0; j < 4; ++j) *reinterpret_cast<u32x4*>(rb + (pslot + 16 * j) * 16) = DP::as_f16(pc[j]);
           if (hwave) {
             // scale 2^(se - 127): the token's largest |h3| of the chunk
             // lands in [2^14, 2^15), within fp16's range
@@ -1087,7 +1103,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
           }
           if (c == 0) SI_TRACE_WAVE(4);
         };
-        u32x4 p0[4], p1[4], p2[4];
+        PT p0[4], p1[4], p2[4];
         uint64_t w0 = 0, w1 = 0, w2 = 0;
         static_assert(kMInflight == 3, "three chunks in flight");
         request(0, p0, w0);
