@@ -973,6 +973,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     SI_TRACE_WAVE(1);
     if (lane == 0 && n_up) atomicAdd(&L.n_up, n_up);
     SI_TRACE_MARK(6);
+    SI_TRACE_WAVE(2);
 
     // ---- 3. down-projection of (tile, the group's rows): per round, wave w
     // takes positions q0 + w + 8 j (j < 8); it requests the tile's W_down^T
@@ -1222,6 +1223,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         if (q0 == 0) SI_TRACE_WAVE(4);
       }
     }
+    SI_TRACE_WAVE(5);
     if (lane == 0 && tile == 0 && n_down) atomicAdd(&L.n_down, n_down);
     if (wv == (mdone ? kOW - 1 : 0) && lane == 0) L.wsum[0] = zok ? 1 : 0;
     // per-wave partial tiles folded in LDS (plain stores; x is no longer
