@@ -965,10 +965,15 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       if (lane < b) st_agent64(&a.h3e[(size_t)row * b + lane], tagged(tag, __float_as_uint(hv)));
       // the next free position of the member's range: the waves that the
       // CU serves first take more rows (with a fixed stride the second wave
-      // of each SIMD finished its rows up to 10 us after the first)
-      int nxt = 0;
-      if (lane == 0) nxt = atomicAdd(&L.gpos, 1);
-      pos = __builtin_amdgcn_readfirstlane(nxt);
+      // of each SIMD finished its rows up to 10 us after the first); with at
+      // most one position per wave there is none, and no wave waits for
+      // the counter
+      int nxt = hi;
+      if (lo + kOW < hi) {
+        if (lane == 0) nxt = atomicAdd(&L.gpos, 1);
+        nxt = __builtin_amdgcn_readfirstlane(nxt);
+      }
+      pos = nxt;
     }
     SI_TRACE_WAVE(1);
     if (lane == 0 && n_up) atomicAdd(&L.n_up, n_up);
