@@ -53,6 +53,8 @@
 // cleared between calls.  Every wait is bounded: past a spin limit the block
 // sets an error bit in the workspace header and goes on without the data.
 
+#include <type_traits>
+
 #include "layer_common.h"
 
 namespace si {
@@ -73,6 +75,7 @@ constexpr int kMaxOwnSub = kMaxOwnRows / kWave;    // 64-row passes of one block
 constexpr int kCountWord = 4 * kMaxOwnSub;         // published word that holds the block's kept count
 constexpr int kMaxPairs = kWave;                   // (owner block, pass) pairs of one group
 constexpr int kMaxChunkRows = 4096;                // kept rows of one group (at most)
+constexpr int kWideGroupRows = 512;                // one token: groups larger than this take 16-piece down rounds
 static_assert(kCountWord < kOwnPubStride, "published words of a block");
 
 // Eight wavefronts per block (two per SIMD), so that a wave may hold up to
@@ -365,7 +368,10 @@ constexpr int kModeInt8 = 2;   // INT8 weights with per-channel scales, x given
 // MODE: the kernel's form (above); each is a separate instance so that the
 // plain form carries none of the others' code (the decoder-block code alone
 // cost the plain form 0.3 us per call)
-template <int BM, int NU, int MODE>
+// WIDE (one token): the down rounds take 16 pieces per wave instead of 8, for
+// groups of more than kWideGroupRows rows (a separate instance: carrying both
+// round widths made the 7B call 0.25 us slower)
+template <int BM, int NU, int MODE, bool WIDE>
 __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
   OwnedLds<BM, NU>& L = *reinterpret_cast<OwnedLds<BM, NU>*>(lds_raw);
@@ -995,7 +1001,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     bool zok = false;
     const int dunit = tile * kWave + lane;
     const bool dcol_ok = dunit < U;
-    constexpr bool kZLane = kODN * BM < kWave;  // wave 0's lane 63 is free for the zero flag
+    constexpr bool kZLane = kODN * BM < kWave && (BM > 1 || 2 * kODN < kWave);  // wave 0's lane 63 is free for the zero flag
     typedef DownPiece<kI8> DP;
     // with 2..8 tokens the rounds are pipelined: once round r's h3 words are
     // in (which also waits for its pieces), round r+1's pieces are requested
@@ -1173,62 +1179,74 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         }
       }
     }
-    if (!pipelined) {
-      for (int q0 = 0; q0 < dN; q0 += kODownRound) {
-        typename DP::type vd[kODN];
-        uint32_t dl = 0;
-#pragma unroll
-        for (int j = 0; j < kODN; ++j) {
-          vd[j] = typename DP::type{};
-          const int q = q0 + wv + kOW * j;
-          if (q < dN) {
-            const uint32_t e = L.dent[q];
-            if ((spec_ok && (e >> 31)) || no_as) {
+    // the unpipelined rounds, kDN pieces per wave and round: 8, and 16 in
+    // the WIDE instance (one token, large groups: a 13B-shaped group keeps
+    // about 66 rows, and with 8 pieces two waves of every block would need a
+    // second round; 16 pieces for the 7B call, about 38 rows per group, made
+    // it 0.9 us slower)
+    auto down_rounds = [&](auto dn) {
+      constexpr int kDN = decltype(dn)::value;
+      static_assert(kDN * BM <= kWave, "a wave polls the h3 words of its pieces, one lane per (piece, token)");
+        for (int q0 = 0; q0 < dN; q0 += kOW * kDN) {
+          typename DP::type vd[kDN];
+          uint32_t dl = 0;
+  #pragma unroll
+          for (int j = 0; j < kDN; ++j) {
+            vd[j] = typename DP::type{};
+            const int q = q0 + wv + kOW * j;
+            if (q < dN) {
+              const uint32_t e = L.dent[q];
+              if ((spec_ok && (e >> 31)) || no_as) {
+                if (dcol_ok) vd[j] = DP::load(a.wdt, e & 0x7fffffffu, U, dunit);
+                dl |= 1u << j;
+              }
+            }
+          }
+          // h3 of (piece j, token t) in lane j * BM + t
+          const int pj = lane / BM, pt = lane - pj * BM;
+          const int pq = q0 + wv + kOW * pj;
+          const bool pok = pj < kDN && pq < dN && pt < b;
+          const bool zlane = kZLane && q0 == 0 && wv == 0 && lane == kWave - 1;
+          const uint64_t* src[1] = {zlane ? &a.zflag[tile]
+                                          : a.h3e + (size_t)(L.dent[pok ? pq : q0] & 0x7fffffffu) * b + (pok ? pt : 0)};
+          uint32_t hw[1];
+          poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
+          if (q0 == 0 && wv == 0) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
+          if (q0 == 0) SI_TRACE_WAVE(3);
+  #pragma unroll
+          for (int j = 0; j < kDN; ++j) {
+            const int q = q0 + wv + kOW * j;
+            float hv[BM];
+            bool nz = false;
+  #pragma unroll
+            for (int t = 0; t < BM; ++t) {
+              hv[t] = (j * BM + t < kWave && q < dN && t < b)
+                          ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(hw[0], min(j * BM + t, kWave - 1)))
+                          : 0.f;
+              nz |= hv[t] != 0.f;
+            }
+            if (q < dN && !((dl >> j) & 1u) && nz) {  // late request
+              const uint32_t e = L.dent[q];
               if (dcol_ok) vd[j] = DP::load(a.wdt, e & 0x7fffffffu, U, dunit);
               dl |= 1u << j;
             }
+            float f[8];
+            DP::values(vd[j], f);
+  #pragma unroll
+            for (int t = 0; t < BM; ++t)
+  #pragma unroll
+              for (int qq = 0; qq < 8; ++qq) acc[t][qq] = fmaf(hv[t], f[qq], acc[t][qq]);
           }
+          n_down += __popc(dl);
+          if (q0 == 0) SI_TRACE_WAVE(4);
         }
-        // h3 of (piece j, token t) in lane j * BM + t
-        const int pj = lane / BM, pt = lane - pj * BM;
-        const int pq = q0 + wv + kOW * pj;
-        const bool pok = pj < kODN && pq < dN && pt < b;
-        const bool zlane = kZLane && q0 == 0 && wv == 0 && lane == kWave - 1;
-        const uint64_t* src[1] = {zlane ? &a.zflag[tile]
-                                        : a.h3e + (size_t)(L.dent[pok ? pq : q0] & 0x7fffffffu) * b + (pok ? pt : 0)};
-        uint32_t hw[1];
-        poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
-        if (q0 == 0 && wv == 0) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
-        if (q0 == 0) SI_TRACE_WAVE(3);
-#pragma unroll
-        for (int j = 0; j < kODN; ++j) {
-          const int q = q0 + wv + kOW * j;
-          float hv[BM];
-          bool nz = false;
-#pragma unroll
-          for (int t = 0; t < BM; ++t) {
-            hv[t] = (j * BM + t < kWave && q < dN && t < b)
-                        ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(hw[0], min(j * BM + t, kWave - 1)))
-                        : 0.f;
-            nz |= hv[t] != 0.f;
-          }
-          if (q < dN && !((dl >> j) & 1u) && nz) {  // late request
-            const uint32_t e = L.dent[q];
-            if (dcol_ok) vd[j] = DP::load(a.wdt, e & 0x7fffffffu, U, dunit);
-            dl |= 1u << j;
-          }
-          float f[8];
-          DP::values(vd[j], f);
-#pragma unroll
-          for (int t = 0; t < BM; ++t)
-#pragma unroll
-            for (int qq = 0; qq < 8; ++qq) acc[t][qq] = fmaf(hv[t], f[qq], acc[t][qq]);
-        }
-        n_down += __popc(dl);
-        if (q0 == 0) SI_TRACE_WAVE(4);
-      }
+    };
+    if (!pipelined) {
+      if constexpr (BM == 1 && WIDE)
+        down_rounds(std::integral_constant<int, 2 * kODN>{});
+      else
+        down_rounds(std::integral_constant<int, kODN>{});
     }
-    SI_TRACE_WAVE(5);
     if (lane == 0 && tile == 0 && n_down) atomicAdd(&L.n_down, n_down);
     if (wv == (mdone ? kOW - 1 : 0) && lane == 0) L.wsum[0] = zok ? 1 : 0;
     // per-wave partial tiles folded in LDS (plain stores; x is no longer
@@ -1334,7 +1352,7 @@ static int owned_rows_per_block(int k, int P, int tiles) {
 
 // Grid of the row-owning kernel on the current device: one block per compute
 // unit, or 0 if its LDS does not fit or one block cannot be resident per CU.
-template <int BM, int NU, int MODE = kModePlain>
+template <int BM, int NU, int MODE = kModePlain, bool WIDE = false>
 static int owned_blocks() {
   static std::atomic<int> cache[kMaxDevices];
   return per_device_once(cache, [](int dev) -> int {
@@ -1343,7 +1361,7 @@ static int owned_blocks() {
       return 0;
     } else {
       int cus = 0, per_cu = 0;
-      const void* fn = reinterpret_cast<const void*>(&k_owned<BM, NU, MODE>);
+      const void* fn = reinterpret_cast<const void*>(&k_owned<BM, NU, MODE, WIDE>);
       if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return -1;
       if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds) != hipSuccess) return -1;
       if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kOT, lds) != hipSuccess) return -1;
@@ -1398,12 +1416,33 @@ static hipError_t owned_b(const LayerCall& c, hipStream_t s) {
     a.h = c.h;
     a.norm_w = c.norm_w;
     a.eps = c.eps;
-    if (mode == kModeInt8)
-      k_owned<BM, NU, kModeInt8><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
-    else if (mode == kModeBlock)
-      k_owned<BM, NU, kModeBlock><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
-    else
-      k_owned<BM, NU, kModePlain><<<P, kOT, owned_lds_bytes<BM, NU>(), s>>>(a);
+    constexpr int lds = owned_lds_bytes<BM, NU>();
+    bool launched = false;
+    if constexpr (BM == 1) {
+      // one token, groups of more than kWideGroupRows rows (more than 64 of
+      // them kept at 12% density): the instance with 16 pieces per down round
+      if (a.tiles * a.R > kWideGroupRows) {
+        const int Pw = mode == kModeInt8    ? owned_blocks<1, NU, kModeInt8, true>()
+                       : mode == kModeBlock ? owned_blocks<1, NU, kModeBlock, true>()
+                                            : owned_blocks<1, NU, kModePlain, true>();
+        if (Pw != P) return hipErrorInvalidConfiguration;
+        if (mode == kModeInt8)
+          k_owned<1, NU, kModeInt8, true><<<P, kOT, lds, s>>>(a);
+        else if (mode == kModeBlock)
+          k_owned<1, NU, kModeBlock, true><<<P, kOT, lds, s>>>(a);
+        else
+          k_owned<1, NU, kModePlain, true><<<P, kOT, lds, s>>>(a);
+        launched = true;
+      }
+    }
+    if (!launched) {
+      if (mode == kModeInt8)
+        k_owned<BM, NU, kModeInt8, false><<<P, kOT, lds, s>>>(a);
+      else if (mode == kModeBlock)
+        k_owned<BM, NU, kModeBlock, false><<<P, kOT, lds, s>>>(a);
+      else
+        k_owned<BM, NU, kModePlain, false><<<P, kOT, lds, s>>>(a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !c.counters || !c.y) return e;
     return launch_sum_counts(a.counts, P, c.n_out, k, c.counters, s);

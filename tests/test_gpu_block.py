@@ -104,6 +104,16 @@ def test_block_7b():
     assert ref["n_gate"] == 1101  # the planted rows: the norm keeps the signs of the token
 
 
+def test_block_13b_large_groups():
+    """At the 13B shape a group holds more than 512 rows, so one token takes
+    the kernel instance with the wider down-projection rounds: gated at
+    alpha = 1 and +inf (every row kept), and non-gated."""
+    c = planted_case(5120, 13824, 0.88, config=4)
+    for alpha in [1.0, math.inf]:
+        c.check(alpha)
+    planted_case(5120, 13824, 0.88, config=4, gated=False).check(1.0)
+
+
 def test_block_non_gated_and_flags():
     c = planted_case(1024, 3000, 0.9, config=3, gated=False)
     for flags in [0, si.SI_NO_AS, si.SI_NO_SPECULATION]:

@@ -433,6 +433,49 @@ def test_13b_layer():
     check_mlp(c, c.x, m_ref, y, cnt)
 
 
+def group_rows(k, d):
+    """Rows of one group of the one-launch kernel: groups of T = ceil(d / 512)
+    blocks over the device's compute units, R rows per block (the rows spread
+    over the grid's whole groups, rounded up to a multiple of 8)."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    T = (d + 511) // 512
+    working = cus // T * T
+    return T * (((k + working - 1) // working + 7) // 8 * 8)
+
+
+@pytest.mark.parametrize("k,d", [(9000, 8192), (40000, 2048)])
+def test_one_token_large_groups(k, d):
+    """One token with groups of more than 512 rows takes the kernel instance
+    with the wider down-projection rounds (16 pieces per wave): every form at
+    alpha = 1 and +inf (all rows kept: the most rounds), a random mask and
+    list, and without speculation.  9000 x 8192 leaves a last group of 40
+    rows; 40000 x 2048 half a group."""
+    assert group_rows(k, d) > 512
+    rng = np.random.default_rng(k + 3 * d)
+    c = Case(rand_bits(rng, (k, d), False), rand_bits(rng, (k, d), False), rand_bits(rng, (d, k), False),
+             rand_bits(rng, (1, d), False))
+    x = to_dev(c.x)
+    for alpha, flags in [(1.0, 0), (math.inf, 0), (1.0, si.SI_NO_SPECULATION), (math.inf, si.SI_NO_SPECULATION)]:
+        print(f"k={k} d={d} alpha={alpha} flags={flags}", flush=True)
+        y, (mask, idx, n, cnt) = c.layer(x, alpha, flags=flags, outputs=True)
+        torch.cuda.synchronize()
+        m_ref = oracle.predict_rows(c.packed, c.x, alpha)[0]
+        assert np.array_equal(mask.cpu().numpy(), m_ref)
+        check_list(idx, n, m_ref)
+        check_mlp(c, c.x, m_ref, y, cnt, flags=flags)
+    m = rng.random(k) < 0.3
+    rows = np.flatnonzero(m).astype(np.int32)
+    y1, c1 = c.layer.sparse_mlp(x, mask=torch.from_numpy(m.astype(np.uint8)).to(DEV), counters=True)
+    torch.cuda.synchronize()
+    check_mlp(c, c.x, m, y1, c1)
+    lst = np.full(k, -1, dtype=np.int32)
+    lst[: rows.size] = rows
+    y2, c2 = c.layer.sparse_mlp(x, None, torch.from_numpy(lst).to(DEV),
+                                torch.tensor([rows.size], dtype=torch.int32, device=DEV), counters=True)
+    torch.cuda.synchronize()
+    check_mlp(c, c.x, m, y2, c2)
+
+
 @pytest.mark.parametrize("k,d,b,one", [(11008, 4096, 1, 1), (13824, 5120, 1, 1), (1376, 512, 1, 1),
                                        (11008, 4096, 2, 1), (1, 128, 1, 1), (65536, 128, 1, 1),
                                        (11008, 4096, 3, 1), (11008, 4096, 8, 1), (13824, 5120, 8, 1),
