@@ -75,7 +75,7 @@ constexpr int kMaxOwnSub = kMaxOwnRows / kWave;    // 64-row passes of one block
 constexpr int kCountWord = 4 * kMaxOwnSub;         // published word that holds the block's kept count
 constexpr int kMaxPairs = kWave;                   // (owner block, pass) pairs of one group
 constexpr int kMaxChunkRows = 4096;                // kept rows of one group (at most)
-constexpr int kWideGroupRows = 512;                // one token: groups larger than this take 16-piece down rounds
+constexpr int kWideGroupRows = 512;                // one token: groups larger than this take wider down batches
 static_assert(kCountWord < kOwnPubStride, "published words of a block");
 
 // Eight wavefronts per block (two per SIMD), so that a wave may hold up to
@@ -88,6 +88,16 @@ constexpr int kFin = kOW - 1;      // the wave that finishes the prediction
 constexpr int kTileWave = kOW - 2; // the wave that initialises the owner's tile of y
 constexpr int kODN = 8;            // W_down^T pieces per wave and down round
 constexpr int kODownRound = kOW * kODN;
+// one token: W_down^T pieces per batch a wave takes, with INT8 weights, and
+// in groups of more than kWideGroupRows rows (measured, us per call:
+// 7B-shaped groups of 384 rows 12.33 / 12.23 / 12.18 / 12.41 with batches of
+// 6 / 8 / 10 / 12, INT8 12.23 / 11.87 / 11.76 / 11.94 / 12.54 with 4 / 6 /
+// 8 / 10 / 16; 13B-shaped groups of 560 rows 17.71 / 17.60 / 18.04 with
+// 10 / 12 / 14)
+constexpr int kODN1 = 10;
+constexpr int kODN1Int8 = 8;
+constexpr int kODN1Wide = 12;
+static_assert(kODN1 < kWave && kODN1Int8 < kWave && kODN1Wide < kWave, "a wave's last lane polls the tile's zero flag");
 static_assert(kODN * kMaxB <= kWave, "a wave polls the h3 words of its pieces, one lane per (piece, token)");
 
 // The down-projection on the matrix cores (4-8 tokens; INT8 pieces are
@@ -163,6 +173,8 @@ struct OwnedLds {
   float nsum[kOW][kMaxB];  // decoder-block mode: per-wave sums of squares of the tokens
   int n_own, n_up, n_down;
   int gpos;  // next gate/up position of the member's range not yet taken by a wave
+  int dpos;    // one token: next down position not yet taken by a wave
+  int issued;  // one token: waves whose first gate/up row is requested
   uint32_t epoch, err;
   uint32_t dmax[2][kMaxB];  // matrix-core down-projection: max |h3| bits per token (chunks alternate)
   float dinv[kMaxB];        // and the inverse of its scale
@@ -368,9 +380,9 @@ constexpr int kModeInt8 = 2;   // INT8 weights with per-channel scales, x given
 // MODE: the kernel's form (above); each is a separate instance so that the
 // plain form carries none of the others' code (the decoder-block code alone
 // cost the plain form 0.3 us per call)
-// WIDE (one token): the down rounds take 16 pieces per wave instead of 8, for
-// groups of more than kWideGroupRows rows (a separate instance: carrying both
-// round widths made the 7B call 0.25 us slower)
+// WIDE (one token): the down batches take kODN1Wide pieces instead of kODN1,
+// for groups of more than kWideGroupRows rows (a separate instance: carrying
+// both batch widths made the 7B call 0.25 us slower)
 template <int BM, int NU, int MODE, bool WIDE>
 __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
@@ -871,7 +883,12 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     }
     const int lo = (n * m) / T, hi = (n * (m + 1)) / T;  // this member's gate/up positions
     const int dN = n;                                     // the down item's positions
-    if (tid == 0) L.gpos = lo + kOW;
+    if (tid == 0) {
+      L.gpos = lo + kOW;
+      L.dpos = 0;
+      L.issued = 0;
+      L.wsum[0] = 0;
+    }
     __syncthreads();
     SI_TRACE_MARK(4);
 
@@ -881,6 +898,19 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     // token's ReLU output is positive.  Each wave works through its rows on
     // its own (no block barrier) and publishes h3 per row and token.
     int n_up = 0;
+    // one token: a wave announces (LDS counter) that its first row's
+    // requests are out, so that the waves without a row can queue their
+    // W_down^T pieces behind them
+    bool first = BM == 1;
+    auto announce = [&]() {
+      if constexpr (BM == 1) {
+        if (first) {
+          asm volatile("" ::: "memory");
+          if (lane == 0) atomicAdd(&L.issued, 1);
+          first = false;
+        }
+      }
+    };
     for (int pos = lo + wv; pos < hi;) {
       const uint32_t e = L.dent[pos];
       const uint32_t row = e & 0x7fffffffu;
@@ -903,6 +933,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
           u32x4 vg[NU8], vu[NU8];
           load_row<NU8>(a.wg + (size_t)urow * U8, U8, ln, vg);
           load_row<NU8>(a.wu + (size_t)urow * U8, U8, ln, vu);
+          announce();
           const float sgv = a.sg[urow], suv = a.su[urow];
           row_dots_i8<BM, NU, true>(vg, vu, L.xs, U8, ln, g, u);
 #pragma unroll
@@ -914,6 +945,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         } else {
           u32x4 vg[NU8];
           load_row<NU8>(a.wg + (size_t)urow * U8, U8, ln, vg);
+          announce();
           const float sgv = a.sg[urow];
           row_dots_i8<BM, NU, false>(vg, vg, L.xs, U8, ln, g, u);
           bool any = false;
@@ -941,12 +973,14 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         u32x4 vg[NU], vu[NU];
         load_row<NU>(a.wg + (size_t)row * U, U, ln, vg);
         load_row<NU>(a.wu + (size_t)row * U, U, ln, vu);
+        announce();
         SI_TRACE_WAVE(0);
         row_dots2<BM, NU>(vg, vu, L.xs, U, ln, g, u);
         up = true;
       } else {
         u32x4 vg[NU];
         load_row<NU>(a.wg + (size_t)row * U, U, ln, vg);
+        announce();
         row_dots<BM, NU>(vg, L.xs, U, ln, g);
         bool any = false;
 #pragma unroll
@@ -1001,7 +1035,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     bool zok = false;
     const int dunit = tile * kWave + lane;
     const bool dcol_ok = dunit < U;
-    constexpr bool kZLane = kODN * BM < kWave && (BM > 1 || 2 * kODN < kWave);  // wave 0's lane 63 is free for the zero flag
+    constexpr bool kZLane = BM == 1 || kODN * BM < kWave;  // lane 63 of a wave's first round is free for the zero flag
     typedef DownPiece<kI8> DP;
     // with 2..8 tokens the rounds are pipelined: once round r's h3 words are
     // in (which also waits for its pieces), round r+1's pieces are requested
@@ -1179,21 +1213,43 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         }
       }
     }
-    // the unpipelined rounds, kDN pieces per wave and round: 8, and 16 in
-    // the WIDE instance (one token, large groups: a 13B-shaped group keeps
-    // about 66 rows, and with 8 pieces two waves of every block would need a
-    // second round; 16 pieces for the 7B call, about 38 rows per group, made
-    // it 0.9 us slower)
+    // the unpipelined rounds, kDN pieces per wave and round (kODN, or with
+    // one token kODN1 / kODN1Int8 / kODN1Wide).  With one token a wave takes kDN
+    // consecutive positions at a time from an LDS counter; a wave without a
+    // gate/up row starts at once, but only after the block's first gate/up
+    // rows are requested (a CU's requests come back in order, and the pieces
+    // must not delay them), and the waves with rows join in as they finish
+    // them (with positions dealt w + 8 j the waves with a gate/up row
+    // requested their pieces only after it, 0.35 us later per 7B call).
+    // With more tokens wave w takes positions q0 + w + 8 j.
     auto down_rounds = [&](auto dn) {
       constexpr int kDN = decltype(dn)::value;
       static_assert(kDN * BM <= kWave, "a wave polls the h3 words of its pieces, one lane per (piece, token)");
-        for (int q0 = 0; q0 < dN; q0 += kOW * kDN) {
+      auto take = [&](int q0) -> int {
+        if constexpr (BM == 1) {
+          int v = 0;
+          if (lane == 0) v = atomicAdd(&L.dpos, kDN);
+          return __builtin_amdgcn_readfirstlane(v);
+        } else {
+          return q0 + kOW * kDN;
+        }
+      };
+      if constexpr (BM == 1) {
+        const int nwork = min(kOW, hi - lo);  // waves with a first gate/up row
+        if (lo + wv >= hi && nwork > 0) {
+          int spins = 0;  // an ordering aid only: the wait may give up
+          while (__hip_atomic_load(&L.issued, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < nwork &&
+                 ++spins < 4096)
+            __builtin_amdgcn_s_sleep(1);
+        }
+      }
+        for (int q0 = BM == 1 ? take(0) : 0; q0 < dN; q0 = take(q0)) {
           typename DP::type vd[kDN];
           uint32_t dl = 0;
   #pragma unroll
           for (int j = 0; j < kDN; ++j) {
             vd[j] = typename DP::type{};
-            const int q = q0 + wv + kOW * j;
+            const int q = BM == 1 ? q0 + j : q0 + wv + kOW * j;
             if (q < dN) {
               const uint32_t e = L.dent[q];
               if ((spec_ok && (e >> 31)) || no_as) {
@@ -1204,18 +1260,19 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
           }
           // h3 of (piece j, token t) in lane j * BM + t
           const int pj = lane / BM, pt = lane - pj * BM;
-          const int pq = q0 + wv + kOW * pj;
+          const int pq = BM == 1 ? q0 + pj : q0 + wv + kOW * pj;
           const bool pok = pj < kDN && pq < dN && pt < b;
-          const bool zlane = kZLane && q0 == 0 && wv == 0 && lane == kWave - 1;
+          const bool zw = q0 == 0 && (BM == 1 || wv == 0);  // the wave that polls the tile's zero flag
+          const bool zlane = kZLane && zw && lane == kWave - 1;
           const uint64_t* src[1] = {zlane ? &a.zflag[tile]
                                           : a.h3e + (size_t)(L.dent[pok ? pq : q0] & 0x7fffffffu) * b + (pok ? pt : 0)};
           uint32_t hw[1];
           poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
-          if (q0 == 0 && wv == 0) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
+          if (zw) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
           if (q0 == 0) SI_TRACE_WAVE(3);
   #pragma unroll
           for (int j = 0; j < kDN; ++j) {
-            const int q = q0 + wv + kOW * j;
+            const int q = BM == 1 ? q0 + j : q0 + wv + kOW * j;
             float hv[BM];
             bool nz = false;
   #pragma unroll
@@ -1243,12 +1300,18 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
     };
     if (!pipelined) {
       if constexpr (BM == 1 && WIDE)
-        down_rounds(std::integral_constant<int, 2 * kODN>{});
+        down_rounds(std::integral_constant<int, kODN1Wide>{});
+      else if constexpr (BM == 1)
+        down_rounds(std::integral_constant<int, kI8 ? kODN1Int8 : kODN1>{});
       else
         down_rounds(std::integral_constant<int, kODN>{});
     }
     if (lane == 0 && tile == 0 && n_down) atomicAdd(&L.n_down, n_down);
-    if (wv == (mdone ? kOW - 1 : 0) && lane == 0) L.wsum[0] = zok ? 1 : 0;
+    if constexpr (BM == 1) {
+      if (zok && lane == 0) L.wsum[0] = 1;  // the wave that took position 0 (the word starts at 0)
+    } else {
+      if (wv == (mdone ? kOW - 1 : 0) && lane == 0) L.wsum[0] = zok ? 1 : 0;
+    }
     // per-wave partial tiles folded in LDS (plain stores; x is no longer
     // needed): kFold waves store, the others add in turn
     constexpr int kFold = OwnedLds<BM, NU>::kFold;
@@ -1419,8 +1482,8 @@ static hipError_t owned_b(const LayerCall& c, hipStream_t s) {
     constexpr int lds = owned_lds_bytes<BM, NU>();
     bool launched = false;
     if constexpr (BM == 1) {
-      // one token, groups of more than kWideGroupRows rows (more than 64 of
-      // them kept at 12% density): the instance with 16 pieces per down round
+      // one token, groups of more than kWideGroupRows rows: the instance with
+      // kODN1Wide pieces per down batch
       if (a.tiles * a.R > kWideGroupRows) {
         const int Pw = mode == kModeInt8    ? owned_blocks<1, NU, kModeInt8, true>()
                        : mode == kModeBlock ? owned_blocks<1, NU, kModeBlock, true>()
