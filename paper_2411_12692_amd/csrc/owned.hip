@@ -1243,6 +1243,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
             __builtin_amdgcn_s_sleep(1);
         }
       }
+        [[maybe_unused]] bool fb = true;  // the wave's first batch (phase-trace marks)
         for (int q0 = BM == 1 ? take(0) : 0; q0 < dN; q0 = take(q0)) {
           typename DP::type vd[kDN];
           uint32_t dl = 0;
@@ -1269,7 +1270,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
           uint32_t hw[1];
           poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
           if (zw) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
-          if (q0 == 0) SI_TRACE_WAVE(3);
+          if (fb) SI_TRACE_WAVE(3);
   #pragma unroll
           for (int j = 0; j < kDN; ++j) {
             const int q = BM == 1 ? q0 + j : q0 + wv + kOW * j;
@@ -1295,7 +1296,8 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
               for (int qq = 0; qq < 8; ++qq) acc[t][qq] = fmaf(hv[t], f[qq], acc[t][qq]);
           }
           n_down += __popc(dl);
-          if (q0 == 0) SI_TRACE_WAVE(4);
+          if (fb) SI_TRACE_WAVE(4);
+          fb = false;
         }
     };
     if (!pipelined) {
@@ -1306,6 +1308,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       else
         down_rounds(std::integral_constant<int, kODN>{});
     }
+    SI_TRACE_WAVE(5);
     if (lane == 0 && tile == 0 && n_down) atomicAdd(&L.n_down, n_down);
     if constexpr (BM == 1) {
       if (zok && lane == 0) L.wsum[0] = 1;  // the wave that took position 0 (the word starts at 0)
