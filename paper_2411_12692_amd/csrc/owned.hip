@@ -1214,9 +1214,9 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       }
     }
     // the unpipelined rounds, kDN pieces per wave and round (kODN, or with
-    // one token kODN1 / kODN1Int8 / kODN1Wide).  With one token a wave takes kDN
-    // consecutive positions at a time from an LDS counter; a wave without a
-    // gate/up row starts at once, but only after the block's first gate/up
+    // one token kODN1 / kODN1Int8 / kODN1Wide).  With one token a wave takes
+    // kDN consecutive positions at a time from an LDS counter; a wave without
+    // a gate/up row starts at once, but only after the block's first gate/up
     // rows are requested (a CU's requests come back in order, and the pieces
     // must not delay them), and the waves with rows join in as they finish
     // them (with positions dealt w + 8 j the waves with a gate/up row
@@ -1243,62 +1243,62 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
             __builtin_amdgcn_s_sleep(1);
         }
       }
-        [[maybe_unused]] bool fb = true;  // the wave's first batch (phase-trace marks)
-        for (int q0 = BM == 1 ? take(0) : 0; q0 < dN; q0 = take(q0)) {
-          typename DP::type vd[kDN];
-          uint32_t dl = 0;
-  #pragma unroll
-          for (int j = 0; j < kDN; ++j) {
-            vd[j] = typename DP::type{};
-            const int q = BM == 1 ? q0 + j : q0 + wv + kOW * j;
-            if (q < dN) {
-              const uint32_t e = L.dent[q];
-              if ((spec_ok && (e >> 31)) || no_as) {
-                if (dcol_ok) vd[j] = DP::load(a.wdt, e & 0x7fffffffu, U, dunit);
-                dl |= 1u << j;
-              }
-            }
-          }
-          // h3 of (piece j, token t) in lane j * BM + t
-          const int pj = lane / BM, pt = lane - pj * BM;
-          const int pq = BM == 1 ? q0 + pj : q0 + wv + kOW * pj;
-          const bool pok = pj < kDN && pq < dN && pt < b;
-          const bool zw = q0 == 0 && (BM == 1 || wv == 0);  // the wave that polls the tile's zero flag
-          const bool zlane = kZLane && zw && lane == kWave - 1;
-          const uint64_t* src[1] = {zlane ? &a.zflag[tile]
-                                          : a.h3e + (size_t)(L.dent[pok ? pq : q0] & 0x7fffffffu) * b + (pok ? pt : 0)};
-          uint32_t hw[1];
-          poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
-          if (zw) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
-          if (fb) SI_TRACE_WAVE(3);
-  #pragma unroll
-          for (int j = 0; j < kDN; ++j) {
-            const int q = BM == 1 ? q0 + j : q0 + wv + kOW * j;
-            float hv[BM];
-            bool nz = false;
-  #pragma unroll
-            for (int t = 0; t < BM; ++t) {
-              hv[t] = (j * BM + t < kWave && q < dN && t < b)
-                          ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(hw[0], min(j * BM + t, kWave - 1)))
-                          : 0.f;
-              nz |= hv[t] != 0.f;
-            }
-            if (q < dN && !((dl >> j) & 1u) && nz) {  // late request
-              const uint32_t e = L.dent[q];
+      [[maybe_unused]] bool fb = true;  // the wave's first batch (phase-trace marks)
+      for (int q0 = BM == 1 ? take(0) : 0; q0 < dN; q0 = take(q0)) {
+        typename DP::type vd[kDN];
+        uint32_t dl = 0;
+#pragma unroll
+        for (int j = 0; j < kDN; ++j) {
+          vd[j] = typename DP::type{};
+          const int q = BM == 1 ? q0 + j : q0 + wv + kOW * j;
+          if (q < dN) {
+            const uint32_t e = L.dent[q];
+            if ((spec_ok && (e >> 31)) || no_as) {
               if (dcol_ok) vd[j] = DP::load(a.wdt, e & 0x7fffffffu, U, dunit);
               dl |= 1u << j;
             }
-            float f[8];
-            DP::values(vd[j], f);
-  #pragma unroll
-            for (int t = 0; t < BM; ++t)
-  #pragma unroll
-              for (int qq = 0; qq < 8; ++qq) acc[t][qq] = fmaf(hv[t], f[qq], acc[t][qq]);
           }
-          n_down += __popc(dl);
-          if (fb) SI_TRACE_WAVE(4);
-          fb = false;
         }
+        // h3 of (piece j, token t) in lane j * BM + t
+        const int pj = lane / BM, pt = lane - pj * BM;
+        const int pq = BM == 1 ? q0 + pj : q0 + wv + kOW * pj;
+        const bool pok = pj < kDN && pq < dN && pt < b;
+        const bool zw = q0 == 0 && (BM == 1 || wv == 0);  // the wave that polls the tile's zero flag
+        const bool zlane = kZLane && zw && lane == kWave - 1;
+        const uint64_t* src[1] = {zlane ? &a.zflag[tile]
+                                        : a.h3e + (size_t)(L.dent[pok ? pq : q0] & 0x7fffffffu) * b + (pok ? pt : 0)};
+        uint32_t hw[1];
+        poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
+        if (zw) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
+        if (fb) SI_TRACE_WAVE(3);
+#pragma unroll
+        for (int j = 0; j < kDN; ++j) {
+          const int q = BM == 1 ? q0 + j : q0 + wv + kOW * j;
+          float hv[BM];
+          bool nz = false;
+#pragma unroll
+          for (int t = 0; t < BM; ++t) {
+            hv[t] = (j * BM + t < kWave && q < dN && t < b)
+                        ? __builtin_bit_cast(float, __builtin_amdgcn_readlane(hw[0], min(j * BM + t, kWave - 1)))
+                        : 0.f;
+            nz |= hv[t] != 0.f;
+          }
+          if (q < dN && !((dl >> j) & 1u) && nz) {  // late request
+            const uint32_t e = L.dent[q];
+            if (dcol_ok) vd[j] = DP::load(a.wdt, e & 0x7fffffffu, U, dunit);
+            dl |= 1u << j;
+          }
+          float f[8];
+          DP::values(vd[j], f);
+#pragma unroll
+          for (int t = 0; t < BM; ++t)
+#pragma unroll
+            for (int qq = 0; qq < 8; ++qq) acc[t][qq] = fmaf(hv[t], f[qq], acc[t][qq]);
+        }
+        n_down += __popc(dl);
+        if (fb) SI_TRACE_WAVE(4);
+        fb = false;
+      }
     };
     if (!pipelined) {
       if constexpr (BM == 1 && WIDE)
