@@ -10,10 +10,11 @@ launch of each graph replay this prints, per point, the median, p10, p90
 and maximum over blocks (or waves) of the time since the earliest block
 started, each the median over several replays.
 
-Usage: ``python -m paper_2411_12692_amd.phase_trace [--batch B] [--replays N]``
+Usage: ``python -m paper_2411_12692_amd.phase_trace [--batch B] [--int8] [--replays N]``
 
 Workloads: one token: the fused call (predict + MLP) on 16 planted 7B-shaped
-layers (d = 4096, k = 11008, s = 0.9, alpha = 1), as ``bench.py`` times it;
+layers (d = 4096, k = 11008, s = 0.9, alpha = 1), as ``bench.py`` times it
+(``--int8``: the same layers quantized to INT8, ``bench.py --mlp int8``);
 B tokens: the mask call over the union of the tokens' planted active sets of
 8 such layers (``bench.py --batch B``).
 """
@@ -52,6 +53,7 @@ def main() -> None:
     ap = argparse.ArgumentParser()
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--replays", type=int, default=8)
+    ap.add_argument("--int8", action="store_true", help="INT8 weights (one token)")
     args = ap.parse_args()
 
     import torch
@@ -69,13 +71,17 @@ def main() -> None:
     L = 16 if b == 1 else 8
     if b == 1:
         pls = [synth.planted_layer(D, K, 0.9, config=2, layer=l, device=dev) for l in range(L)]
-        layers = [si.MLPLayer(p.w_gate, p.w_up, p.w_down) for p in pls]
+        if args.int8:
+            layers = [si.Int8MLPLayer(p.w_gate, p.w_up, p.w_down) for p in pls]
+        else:
+            layers = [si.MLPLayer(p.w_gate, p.w_up, p.w_down) for p in pls]
         xs = [p.x for p in pls]
         y = torch.empty(1, D, dtype=torch.float32, device=dev)
 
         def call(i):
             layers[i % L](xs[i % L], 1.0, y=y)
-        what = f"fused call, 7B layer (d={D}, k={K}), planted s=0.9, alpha=1, 1 token, pool of {L} layers"
+        what = (f"fused call, 7B layer (d={D}, k={K}){', INT8 weights' if args.int8 else ''}, planted s=0.9, "
+                f"alpha=1, 1 token, pool of {L} layers")
     else:
         pls = [synth.planted_layer(D, K, 0.9, config=5, layer=l, device=dev) for l in range(L)]
         layers = [si.MLPLayer(p.w_gate, p.w_up, p.w_down, max_batch=b) for p in pls]
