@@ -888,6 +888,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       L.dpos = 0;
       L.issued = 0;
       L.wsum[0] = 0;
+      if constexpr (BM == 1 && kI8) L.wsum[1] = 0;  // waves done with their gate/up rows
     }
     __syncthreads();
     SI_TRACE_MARK(4);
@@ -1016,6 +1017,9 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       pos = nxt;
     }
     SI_TRACE_WAVE(1);
+    if constexpr (BM == 1 && kI8) {
+      if (lane == 0 && lo + wv < hi) atomicAdd(&L.wsum[1], 1);
+    }
     if (lane == 0 && n_up) atomicAdd(&L.n_up, n_up);
     SI_TRACE_MARK(6);
     SI_TRACE_WAVE(2);
@@ -1268,6 +1272,22 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         const uint64_t* src[1] = {zlane ? &a.zflag[tile]
                                         : a.h3e + (size_t)(L.dent[pok ? pq : q0] & 0x7fffffffu) * b + (pok ? pt : 0)};
         uint32_t hw[1];
+        if constexpr (BM == 1 && kI8) {
+          // INT8 rows: a wave without gate/up rows polls its first batch's
+          // h3 words once the block's own gate/up rows are done (the half-size
+          // pieces are in long before the words are published, and a poll
+          // that comes back without them costs a round trip: 11.72 -> 11.48
+          // us per 7B call; with fp16 rows the pieces come in after the
+          // words, and the same wait cost the non-gated and 13B-shaped calls
+          // 0.1 us)
+          if (fb && lo + wv >= hi) {
+            const int nwork = min(kOW, hi - lo);
+            int spins = 0;  // bounded: the wait only orders the poll
+            while (__hip_atomic_load(&L.wsum[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) < nwork &&
+                   ++spins < 65536)
+              __builtin_amdgcn_s_sleep(1);
+          }
+        }
         poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
         if (zw) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
         if (fb) SI_TRACE_WAVE(3);
