@@ -260,9 +260,10 @@ def time_steps(step, steps, warmup):
     ``steps`` launches (step i runs layer i mod pool, continuing the
     rotation), uploaded to the device before the replay.  Events on the
     replay stream bracket the one replay, with a synchronization on both
-    sides; the time includes the replay's own start (about 20 us per replay on
-    the MI355X, so short runs read slower).  Returns (us per step, wall us
-    per step)."""
+    sides.  A spin kernel of about 0.2 ms is queued ahead of the start event,
+    so that the host's submission of the replay (about 20 us, which a decode
+    loop hides behind the previous token's work) happens while the device is
+    busy and stays out of the timed region.  Returns us per step."""
     import torch
 
     stream = torch.cuda.Stream()
@@ -278,15 +279,15 @@ def time_steps(step, steps, warmup):
     upload_graph(graph, stream)
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
-    t0 = time.perf_counter()
+    with torch.cuda.stream(stream):
+        torch.cuda._sleep(int(2.4e9 * 2e-4))
     e0.record(stream)
     with torch.cuda.stream(stream):
         graph.replay()
     e1.record(stream)
     torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
     del graph
-    return e0.elapsed_time(e1) * 1e3 / steps, wall * 1e6 / steps
+    return e0.elapsed_time(e1) * 1e3 / steps
 
 
 def truth_counts(mask, x, w_gate, w_up):
@@ -853,12 +854,12 @@ def main():
     read_bytes = sum(algorithmic_bytes(K_, D_, B_, *c, block=block, int8=int8) for c in reads) / L
 
     steps, warmup = args.steps, args.warmup
-    us_per_layer, wall_us = time_steps(step, steps, warmup)
-    print(f"# timed {steps} steps after {warmup} warm-up steps: {us_per_layer:.3f} us/layer (wall {wall_us:.3f})",
+    us_per_layer = time_steps(step, steps, warmup)
+    print(f"# timed {steps} steps after {warmup} warm-up steps: {us_per_layer:.3f} us/layer",
           file=sys.stderr, flush=True)
     plain_us = None
     if block:  # the same layers through the plain call (x given, no residual), for comparison
-        plain_us, _ = time_steps(lambda i: layers[i % L](xs[i % L], args.alpha, y=ys[i % L]), steps, warmup)
+        plain_us = time_steps(lambda i: layers[i % L](xs[i % L], args.alpha, y=ys[i % L]), steps, warmup)
         print(f"# plain call on the same layers: {plain_us:.3f} us/layer", file=sys.stderr, flush=True)
     peak = measured_read_peak(si, dev) if not args.no_peak else None
     if peak:
