@@ -87,7 +87,6 @@ constexpr int kOSignUnits = (kMaxD / 128 + kOW - 1) / kOW;  // sign units per wa
 constexpr int kFin = kOW - 1;      // the wave that finishes the prediction
 constexpr int kTileWave = kOW - 2; // the wave that initialises the owner's tile of y
 constexpr int kODN = 8;            // W_down^T pieces per wave and down round
-constexpr int kODownRound = kOW * kODN;
 // one token: W_down^T pieces per batch a wave takes, with INT8 weights, and
 // in groups of more than kWideGroupRows rows (measured, us per call:
 // 7B-shaped groups of 384 rows 12.33 / 12.23 / 12.18 / 12.41 with batches of
@@ -1168,21 +1167,27 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
       }
     }
     if constexpr (BM >= 2 && !kMfma) {
-      if (spec_ok && dN > 0) {
-        pipelined = true;
+      // a down item that one round of kODN pieces per wave does not cover but
+      // one of 12 does takes that single round, all others pipelined rounds of
+      // kODN (two tokens, the union of planted sets at s = 0.9, about 72
+      // positions per group: 16.9 -> 15.9 us per 7B call; rounds of 12 for
+      // every item made the longer items of the fused call and of s = 0.5
+      // 0.6-1.5 us slower, and the shorter ones of s = 0.95-0.97 1 us slower)
+      auto piped = [&](auto pn) {
+        constexpr int kPN = decltype(pn)::value, kPRound = kOW * kPN;
         const int dcu = min(dunit, U - 1);  // column unit of the loads (in the row even past d)
-        typename DP::type va[kODN], vb[kODN];
-        auto request = [&](int q0, typename DP::type(&v)[kODN]) {
+        typename DP::type va[kPN], vb[kPN];
+        auto request = [&](int q0, typename DP::type(&v)[kPN]) {
 #pragma unroll
-          for (int j = 0; j < kODN; ++j) {
+          for (int j = 0; j < kPN; ++j) {
             const int q = min(q0 + wv + kOW * j, dN - 1);
             v[j] = DP::load(a.wdt, L.dent[q] & 0x7fffffffu, U, dcu);
           }
         };
-        auto round = [&](int q0, typename DP::type(&cur)[kODN], typename DP::type(&nxt)[kODN]) {
+        auto round = [&](int q0, typename DP::type(&cur)[kPN], typename DP::type(&nxt)[kPN]) {
           const int pj = lane / BM, pt = lane - pj * BM;
           const int pq = q0 + wv + kOW * pj;
-          const bool pok = pj < kODN && pq < dN && pt < b;
+          const bool pok = pj < kPN && pq < dN && pt < b;
           const bool zlane = kZLane && q0 == 0 && wv == 0 && lane == kWave - 1;
           const uint64_t* src[1] = {zlane ? &a.zflag[tile]
                                           : a.h3e + (size_t)(L.dent[pok ? pq : q0] & 0x7fffffffu) * b + (pok ? pt : 0)};
@@ -1190,9 +1195,9 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
           poll_words<1>(src, (pok || zlane) ? 1 : 0, tag, a.hdr, hw);
           if (q0 == 0 && wv == 0) zok = __builtin_amdgcn_readlane(hw[0], kWave - 1) == 1u && kZLane;
           if (q0 == 0) SI_TRACE_WAVE(3);
-          if (q0 + kODownRound < dN) request(q0 + kODownRound, nxt);
+          if (q0 + kPRound < dN) request(q0 + kPRound, nxt);
 #pragma unroll
-          for (int j = 0; j < kODN; ++j) {
+          for (int j = 0; j < kPN; ++j) {
             const int q = q0 + wv + kOW * j;
             float hv[BM];
 #pragma unroll
@@ -1211,10 +1216,17 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
           if (q0 == 0) SI_TRACE_WAVE(4);
         };
         request(0, va);
-        for (int q0 = 0; q0 < dN; q0 += 2 * kODownRound) {
+        for (int q0 = 0; q0 < dN; q0 += 2 * kPRound) {
           round(q0, va, vb);
-          if (q0 + kODownRound < dN) round(q0 + kODownRound, vb, va);
+          if (q0 + kPRound < dN) round(q0 + kPRound, vb, va);
         }
+      };
+      if (spec_ok && dN > 0) {
+        pipelined = true;
+        if (dN > kOW * kODN && dN <= kOW * 12)
+          piped(std::integral_constant<int, 12>{});
+        else
+          piped(std::integral_constant<int, kODN>{});
       }
     }
     // the unpipelined rounds, kDN pieces per wave and round (kODN, or with
