@@ -103,8 +103,11 @@ size_t si_signs_bytes(int k, int d);
 si_status si_pack_signs(const uint16_t* w_gate, int k, int d, uint32_t* signs, void* stream);
 
 /*
- * Export packed signs in the canonical layout: out[i][w] (k rows of d/32
- * uint32) has bit j set iff W_gate[i][32*w + j] has its sign bit set.
+ * Export packed signs in the canonical layout of Section IV-B 1) (each row's
+ * sign bits packed 32 to a word, in element order): out[i][w] (k rows of
+ * d/32 uint32, written) has bit j set iff W_gate[i][32*w + j] has its sign
+ * bit set.  signs: si_signs_bytes(k, d) bytes from si_pack_signs, read.
+ * For tests and inspection; the decode path never calls it.
  */
 si_status si_signs_to_canonical(const uint32_t* signs, int k, int d, uint32_t* out, void* stream);
 
@@ -127,7 +130,10 @@ si_status si_transpose_down(const uint16_t* w_down, int d, int k, uint16_t* w_do
 int32_t si_alpha_threshold(float alpha, int d);
 
 /* Bytes of workspace needed by si_predict / si_sparse_mlp /
- * si_predict_sparse_mlp for these shapes (0 for unsupported shapes). */
+ * si_predict_sparse_mlp for these shapes (0 for unsupported shapes): the
+ * scratch of the compaction (Section IV-B 2)) and of the h3 values handed
+ * from the gate/up step to the down-projection (Eq. (1), steps 3 and 4)
+ * between blocks, plus the call counter and error bits.  Host-only. */
 size_t si_workspace_bytes(int k, int d, int b);
 
 /*
@@ -230,7 +236,8 @@ si_status si_sparse_mlp(const uint16_t* w_gate, const uint16_t* w_up, const uint
 
 /*
  * 1 if si_predict, si_sparse_mlp and si_predict_sparse_mlp (and their
- * non-gated forms) run as a single kernel launch for these shapes on the
+ * non-gated forms), the steps of Section IV-B for one layer, run as a
+ * single kernel launch for these shapes on the
  * current device: at most 256 rows of W_gate per compute unit (k <= 65536 on
  * a 256-CU MI355X) and one block with 96-160 KB of LDS resident on every
  * compute unit; 0 if they take the multi-launch path (same results) or the
