@@ -131,9 +131,10 @@ int32_t si_alpha_threshold(float alpha, int d);
 
 /* Bytes of workspace needed by si_predict / si_sparse_mlp /
  * si_predict_sparse_mlp for these shapes (0 for unsupported shapes): the
- * scratch of the compaction (Section IV-B 2)) and of the h3 values handed
- * from the gate/up step to the down-projection (Eq. (1), steps 3 and 4)
- * between blocks, plus the call counter and error bits.  Host-only. */
+ * scratch of the prediction's outputs handed between blocks (Section IV-B
+ * 2)), of the h3 values handed from the gate/up step to the down-projection
+ * (Eq. (1), steps 3 and 4; Section IV-B 3), 4)), and the call counter and
+ * error bits.  Host-only. */
 size_t si_workspace_bytes(int k, int d, int b);
 
 /*
