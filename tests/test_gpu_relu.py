@@ -145,6 +145,16 @@ def test_relu_batches(b):
         check(c, m_ref, y2, cnt2)
 
 
+def test_relu_one_token_large_groups():
+    """One token in groups of more than 512 rows (k = 20000 at d = 4096:
+    groups of 8 blocks x 80 rows) takes the kernel instance with the wider
+    down-projection batches: the planted construction at alpha = 1 and
+    +inf, and without speculation."""
+    c = ReluCase.planted(4096, 20000, 0.9, config=6)
+    for alpha, flags in [(1.0, 0), (math.inf, 0), (1.0, si.SI_NO_SPECULATION)]:
+        fused(c, alpha, flags)
+
+
 @pytest.mark.parametrize("k,d,b,one", [(1, 128, 1, 1), (65, 384, 2, 1), (129, 8192, 3, 1), (20000, 384, 1, 1),
                                        (65537, 128, 1, 0)])
 def test_relu_edge_shapes(k, d, b, one):
