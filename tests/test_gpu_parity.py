@@ -285,6 +285,28 @@ def test_batch_union(b):
         check_mlp(c, c.x, m_ref, y, cnt)
 
 
+@pytest.mark.parametrize("k,d,b", [(1000, 640, 3), (1000, 640, 4), (2500, 1152, 3), (700, 8192, 4)])
+def test_batch_token_staging_ragged(k, d, b):
+    """3-4 tokens, whose token block is copied from memory straight into LDS:
+    units past d (d = 640: 80 units of 128 per token; d = 1152: 144 of 192)
+    and the missing fourth token must read as zero in every form."""
+    rng = np.random.default_rng(k + d + 31 * b)
+    c = Case(rand_bits(rng, (k, d), False), rand_bits(rng, (k, d), False), rand_bits(rng, (d, k), False),
+             rand_bits(rng, (b, d), False), max_batch=b)
+    x = to_dev(c.x)
+    for alpha in [1.0, math.inf]:
+        m_ref = check_predict(c, c.x, alpha)
+        y, (mask, idx, n, cnt) = c.layer(x, alpha, outputs=True)
+        torch.cuda.synchronize()
+        assert np.array_equal(mask.cpu().numpy(), m_ref)
+        check_list(idx, n, m_ref)
+        check_mlp(c, c.x, m_ref, y, cnt)
+    m = rng.random(k) < 0.4
+    y1, c1 = c.layer.sparse_mlp(x, mask=torch.from_numpy(m.astype(np.uint8)).to(DEV), counters=True)
+    torch.cuda.synchronize()
+    check_mlp(c, c.x, m, y1, c1)
+
+
 @pytest.mark.parametrize("b", [4, 5, 8])
 def test_batch_7b_fused(b):
     """The fused call at the 7B shape with 4 to 8 tokens.  With 5 or more,
