@@ -109,7 +109,7 @@ static_assert(kODN * kMaxB <= kWave, "a wave polls the h3 words of its pieces, o
 // into two fp16 parts (hi + lo), so the products keep fp32 precision for any
 // finite h3.
 constexpr int kMRows = 32;                // rows per chunk
-constexpr int kMInflight = 3;             // chunks whose pieces are in flight
+constexpr int kMInflight = 3;             // chunks whose pieces are in flight (3-4 tokens; one more with 5-8)
 constexpr int kMPitch = kTile * 2 + 32;   // bytes per row of a chunk in LDS (padded against bank conflicts)
 constexpr int kMTok = 16;                 // tokens of the MFMA (b <= 8 used)
 static_assert(kMRows == 4 * kOW, "each wave stages 4 rows of a chunk (16 lanes per row)");
@@ -1087,6 +1087,9 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
         mdone = true;
         MfmaLds<BM>& M = *reinterpret_cast<MfmaLds<BM>*>(L.mf_raw);
         const int nch = (dN + kMRows - 1) / kMRows;
+        // chunks in flight: 4 with 5-8 tokens (the fused 8-token call 58.6 ->
+        // 57.7 us), 3 with 3-4 (4 made the 4-token call 0.4 us slower)
+        constexpr int kMI = BM >= 8 ? kMInflight + 1 : kMInflight;
         // pieces: the thread stages row 4 wv + lane / 16 of each chunk, its
         // 16-byte units lane % 16 + 16 j (j < 4) of the tile
         const int prow = 4 * wv + (lane >> 4), pslot = lane & 15;
@@ -1153,7 +1156,7 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
               const int hlf = i / ((kMTok - BM) * kMRows), r = i - hlf * ((kMTok - BM) * kMRows);
               M.bop[hlf][BM + r / kMRows][r % kMRows] = 0;
             }
-          if (c + kMInflight < nch) request(c + kMInflight, pc, w);
+          if (c + kMI < nch) request(c + kMI, pc, w);
           __syncthreads();
           // lane (g = lane / 16, j16 = lane % 16): B = token j16's rows
           // 8 g .. 8 g + 7; A = those rows of column j16 of the block, from
@@ -1183,16 +1186,31 @@ __global__ __launch_bounds__(kOT) void k_owned(OwnedArgs a) {
           }
           if (c == 0) SI_TRACE_WAVE(4);
         };
-        PT p0[4], p1[4], p2[4];
-        uint64_t w0 = 0, w1 = 0, w2 = 0;
-        static_assert(kMInflight == 3, "three chunks in flight");
-        request(0, p0, w0);
-        if (1 < nch) request(1, p1, w1);
-        if (2 < nch) request(2, p2, w2);
-        for (int c = 0; c < nch; c += kMInflight) {
-          chunk(c, p0, w0);
-          if (c + 1 < nch) chunk(c + 1, p1, w1);
-          if (c + 2 < nch) chunk(c + 2, p2, w2);
+        if constexpr (kMI == 4) {
+          PT p0[4], p1[4], p2[4], p3[4];
+          uint64_t w0 = 0, w1 = 0, w2 = 0, w3 = 0;
+          request(0, p0, w0);
+          if (1 < nch) request(1, p1, w1);
+          if (2 < nch) request(2, p2, w2);
+          if (3 < nch) request(3, p3, w3);
+          for (int c = 0; c < nch; c += kMI) {
+            chunk(c, p0, w0);
+            if (c + 1 < nch) chunk(c + 1, p1, w1);
+            if (c + 2 < nch) chunk(c + 2, p2, w2);
+            if (c + 3 < nch) chunk(c + 3, p3, w3);
+          }
+        } else {
+          PT p0[4], p1[4], p2[4];
+          uint64_t w0 = 0, w1 = 0, w2 = 0;
+          static_assert(kMI == 3, "three chunks in flight");
+          request(0, p0, w0);
+          if (1 < nch) request(1, p1, w1);
+          if (2 < nch) request(2, p2, w2);
+          for (int c = 0; c < nch; c += kMI) {
+            chunk(c, p0, w0);
+            if (c + 1 < nch) chunk(c + 1, p1, w1);
+            if (c + 2 < nch) chunk(c + 2, p2, w2);
+          }
         }
         n_down = wv == 0 ? dN : 0;
       }
