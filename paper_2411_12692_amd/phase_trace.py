@@ -10,13 +10,14 @@ launch of each graph replay this prints, per point, the median, p10, p90
 and maximum over blocks (or waves) of the time since the earliest block
 started, each the median over several replays.
 
-Usage: ``python -m paper_2411_12692_amd.phase_trace [--batch B] [--int8] [--replays N]``
+Usage: ``python -m paper_2411_12692_amd.phase_trace [--batch B] [--int8] [--shape 7b|13b] [--replays N]``
 
 Workloads: one token: the fused call (predict + MLP) on 16 planted 7B-shaped
 layers (d = 4096, k = 11008, s = 0.9, alpha = 1), as ``bench.py`` times it
-(``--int8``: the same layers quantized to INT8, ``bench.py --mlp int8``);
-B tokens: the mask call over the union of the tokens' planted active sets of
-8 such layers (``bench.py --batch B``).
+(``--int8``: the same layers quantized to INT8, ``bench.py --mlp int8``;
+``--shape 13b``: 13B-shaped layers, d = 5120, k = 13824, s = 0.88,
+``bench.py --shape 13b``); B tokens: the mask call over the union of the
+tokens' planted active sets of 8 7B-shaped layers (``bench.py --batch B``).
 """
 
 from __future__ import annotations
@@ -54,7 +55,10 @@ def main() -> None:
     ap.add_argument("--batch", type=int, default=1)
     ap.add_argument("--replays", type=int, default=8)
     ap.add_argument("--int8", action="store_true", help="INT8 weights (one token)")
+    ap.add_argument("--shape", choices=("7b", "13b"), default="7b", help="layer shape (one token)")
     args = ap.parse_args()
+    if args.shape != "7b" and args.batch != 1:
+        raise SystemExit("--shape 13b is a one-token workload")
 
     import torch
 
@@ -67,10 +71,11 @@ def main() -> None:
     import paper_2411_12692_amd as si
 
     dev = torch.device("cuda:0")
-    D, K, b = 4096, 11008, args.batch
+    D, K, S, cfg = (5120, 13824, 0.88, 4) if args.shape == "13b" else (4096, 11008, 0.9, 2)
+    b = args.batch
     L = 16 if b == 1 else 8
     if b == 1:
-        pls = [synth.planted_layer(D, K, 0.9, config=2, layer=l, device=dev) for l in range(L)]
+        pls = [synth.planted_layer(D, K, S, config=cfg, layer=l, device=dev) for l in range(L)]
         if args.int8:
             layers = [si.Int8MLPLayer(p.w_gate, p.w_up, p.w_down) for p in pls]
         else:
@@ -80,8 +85,8 @@ def main() -> None:
 
         def call(i):
             layers[i % L](xs[i % L], 1.0, y=y)
-        what = (f"fused call, 7B layer (d={D}, k={K}){', INT8 weights' if args.int8 else ''}, planted s=0.9, "
-                f"alpha=1, 1 token, pool of {L} layers")
+        what = (f"fused call, {args.shape.upper()} layer (d={D}, k={K}){', INT8 weights' if args.int8 else ''}, "
+                f"planted s={S}, alpha=1, 1 token, pool of {L} layers")
     else:
         pls = [synth.planted_layer(D, K, 0.9, config=5, layer=l, device=dev) for l in range(L)]
         layers = [si.MLPLayer(p.w_gate, p.w_up, p.w_down, max_batch=b) for p in pls]
