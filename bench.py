@@ -260,10 +260,14 @@ def time_steps(step, steps, warmup):
     ``steps`` launches (step i runs layer i mod pool, continuing the
     rotation), uploaded to the device before the replay.  Events on the
     replay stream bracket the one replay, with a synchronization on both
-    sides.  A spin kernel of about 0.2 ms is queued ahead of the start event,
+    sides.  A spin kernel of about 5 ms is queued ahead of the start event,
     so that the host's submission of the replay (about 20 us, which a decode
     loop hides behind the previous token's work) happens while the device is
-    busy and stays out of the timed region.  Returns us per step."""
+    busy and stays out of the timed region, and so that the device's clocks
+    are at their busy level when the replay starts, as in a decode loop that
+    never idles (after the host's synchronization they have dropped; 0.2 ms
+    of spinning left a 20-step replay about 0.2 us per step slower).
+    Returns us per step."""
     import torch
 
     stream = torch.cuda.Stream()
@@ -280,7 +284,7 @@ def time_steps(step, steps, warmup):
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     with torch.cuda.stream(stream):
-        torch.cuda._sleep(int(2.4e9 * 2e-4))
+        torch.cuda._sleep(int(2.4e9 * 5e-3))
     e0.record(stream)
     with torch.cuda.stream(stream):
         graph.replay()
