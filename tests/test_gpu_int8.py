@@ -219,6 +219,32 @@ def test_int8_edge_shapes(k, d, b):
             check(c, m_ref, y, cnt)
 
 
+@pytest.mark.parametrize("k,d,gated", [(9000, 8192, True), (40000, 2048, True), (20000, 4096, False)])
+def test_int8_one_token_large_groups(k, d, gated):
+    """One token with groups of more than 512 rows (T = ceil(d / 512) blocks
+    of R rows, R the rows over the grid's whole groups rounded up to a
+    multiple of 8) takes the INT8 instance with the wider down batches:
+    alpha = 1 and +inf (every row kept: the most batches), without
+    speculation, and a random mask.  9000 x 8192 leaves a last group of 40
+    rows, 40000 x 2048 half a group; 20000 x 4096 is the non-gated form."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    T = (d + 511) // 512
+    working = cus // T * T
+    assert T * (((k + working - 1) // working + 7) // 8 * 8) > 512
+    rng = np.random.default_rng(k + 5 * d)
+    c = I8Case(rand_bits(rng, (k, d)), rand_bits(rng, (k, d)) if gated else None, rand_bits(rng, (d, k)),
+               rand_bits(rng, (1, d)))
+    check_weights(c)
+    assert si._lib.load().si_single_launch(c.k, c.d, 1) == 1
+    for alpha, flags in [(1.0, 0), (math.inf, 0), (1.0, si.SI_NO_SPECULATION)]:
+        print(f"k={k} d={d} gated={gated} alpha={alpha} flags={flags}", flush=True)
+        fused(c, alpha, flags)
+    m = rng.random(k) < 0.3
+    y, cnt = c.layer.sparse_mlp(to_dev(c.x), torch.from_numpy(m.astype(np.uint8)).to(DEV), counters=True)
+    torch.cuda.synchronize()
+    check(c, m, y, cnt)
+
+
 @pytest.mark.parametrize("seed", range(8))
 def test_int8_random_shapes(seed):
     """Seeded random shapes (d a multiple of 128 up to 8192, k up to 12000,

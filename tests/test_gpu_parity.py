@@ -468,7 +468,7 @@ def group_rows(k, d):
 @pytest.mark.parametrize("k,d", [(9000, 8192), (40000, 2048)])
 def test_one_token_large_groups(k, d):
     """One token with groups of more than 512 rows takes the kernel instance
-    with the wider down-projection rounds (16 pieces per wave): every form at
+    with the wider down batches (12 pieces instead of 10): every form at
     alpha = 1 and +inf (all rows kept: the most rounds), a random mask and
     list, and without speculation.  9000 x 8192 leaves a last group of 40
     rows; 40000 x 2048 half a group."""
