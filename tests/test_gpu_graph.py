@@ -4,9 +4,11 @@ The benchmark times the path from graph replays, and the kernels keep a call
 counter in the workspace on the device (the tags of the exchange words), so
 replays of one captured call must behave like fresh calls.  A graph of calls
 over several layers (fp16 gated, non-gated, INT8 and decoder-block forms, at
-one and three tokens) is replayed several times, with eager calls on the same
-workspaces in between; masks, kept lists and counts must equal the eager
-call's bit for bit and y must match it to fp32 summation order.
+one and three tokens; and one token at the 13B shape, whose groups of more
+than 512 rows take the instance with the wider down batches) is replayed
+several times, with eager calls on the same workspaces in between; masks,
+kept lists and counts must equal the eager call's bit for bit and y must
+match it to fp32 summation order.
 """
 
 import numpy as np
@@ -21,8 +23,7 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda"
 
 
-def make_layers(form, b, n_layers=3):
-    d, k = 1024, 2752
+def make_layers(form, b, n_layers=3, d=1024, k=2752):
     out = []
     for l in range(n_layers):
         pl = synth.planted_layer(d, k, 0.9, config=9, layer=l, device=DEV)
@@ -54,7 +55,17 @@ def snapshot(res):
 @pytest.mark.parametrize("form", ["gated", "relu", "int8", "block"])
 @pytest.mark.parametrize("b", [1, 3])
 def test_graph_replays_match_eager(form, b):
-    layers = make_layers(form, b)
+    replay_and_compare(form, b, make_layers(form, b))
+
+
+@pytest.mark.parametrize("form", ["gated", "int8", "block"])
+def test_graph_replays_large_groups(form):
+    # 13B shape: on 256 compute units, groups of 10 blocks x 56 rows = 560 rows
+    replay_and_compare(form, 1, make_layers(form, 1, d=5120, k=13824))
+
+
+def replay_and_compare(form, b, layers):
+    print(f"form={form} b={b} d={layers[0][1].shape[1]}", flush=True)
     ys = [torch.empty(b, layers[0][1].shape[1], dtype=torch.float32, device=DEV) for _ in layers]
     eager = []
     for (layer, x, h, nw), y in zip(layers, ys):
