@@ -21,6 +21,11 @@ kernel's summation tree: 64 (the hi and lo products of a chunk of 32 rows)
 groups of up to 6 chunks (more than the 3 in flight), a ragged last chunk and
 a ragged last tile of y (d = 640).  Dropping the lo part (2^-12 per term)
 exceeds this bound (checked on the CPU in ``tests/test_down_bound.py``).
+With one token h3 stays fp32 and a wave takes down batches as they come, so
+a lane may sum every row of its group: D is then the group's rows + the 8
+waves' partial tiles + the groups + 2 (the representation terms only widen
+the bound).  The one-token cases include groups of 640 rows (d = 2048, k =
+40000), which take the instance with the wider down batches.
 """
 
 import numpy as np
@@ -55,16 +60,21 @@ def one_hot_tokens(rng, b, d):
     return x.view(np.uint16)
 
 
-def group_depth(k, d, cus):
+def group_depth(k, d, cus, b=8):
     """Depth of the summation tree of one y element in the row-owning kernel:
     the blocks form groups of T = ceil(d / 512) and own R rows each (the rows
     spread over the grid's whole groups, rounded up to a multiple of 8), a
-    group's T R rows are summed in chunks of 32, the groups' tiles into y."""
+    group's T R rows are summed in chunks of 32 (b > 1; with one token a lane
+    may sum all of them, then the 8 waves' partial tiles), the groups' tiles
+    into y."""
     T = (d + 511) // 512
     working = cus // T * T
     R = ((k + working - 1) // working + 7) // 8 * 8
     rows = R * T
-    return 64 + (rows + 31) // 32 + (k + rows - 1) // rows + 2
+    groups = (k + rows - 1) // rows
+    if b == 1:
+        return rows + 8 + groups + 2
+    return 64 + (rows + 31) // 32 + groups + 2
 
 
 def y_bound(h3, WdT, depth):
@@ -85,6 +95,8 @@ CASES = [
     (4096, 3001, 4, "mask", 0),
     (640, 21000, 8, "mask", si.SI_NO_SPECULATION),  # the fp32 rounds, same bound
     (640, 21000, 2, "mask", 0),
+    (640, 21000, 1, "mask", 0),  # one token: fp32 h3 and down
+    (2048, 40000, 1, "fused", 0),  # one token, groups of 640 rows
 ]
 
 
@@ -114,7 +126,7 @@ def test_down_wide_h3_range(d, k, b, form, flags):
     yg = y.cpu().numpy().astype(np.float64)
     err = np.abs(yg - out["y"])
     keep = oracle.active_rows(mask)
-    depth = group_depth(k, d, torch.cuda.get_device_properties(0).multi_processor_count)
+    depth = group_depth(k, d, torch.cuda.get_device_properties(0).multi_processor_count, b)
     bound = y_bound(out["h3"][:, keep], oracle.fp16_to_f64(wd[:, keep]).T, depth)
     bad = err > bound
     if bad.any():
