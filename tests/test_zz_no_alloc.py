@@ -3,11 +3,12 @@
 per-device scratch array in place of a caller's workspace) against the
 workspace form ``si_predict_sparse_mlp`` and the oracle.
 
-Three calls in a row on the one scratch array, each smaller or different in
-shape from the one before (a 7B-shaped layer with 2 tokens, the small
-planted block with 1 token, then a ragged random shape with 3 tokens), so
-that whatever a call leaves in the array cannot pass for the next call's
-data.  Masks, kept lists, counts and work counters bit-exact against the
+Four calls in a row on the one scratch array, each smaller or different in
+shape from the one before (a 13B-shaped layer with 1 token, whose groups of
+more than 512 rows take the instance with the wider down batches, a
+7B-shaped layer with 2 tokens, the small planted block with 1 token, then a
+ragged random shape with 3 tokens), so that whatever a call leaves in the
+array cannot pass for the next call's data.  Masks, kept lists, counts and work counters bit-exact against the
 workspace form (and the masks, lists and counts against the oracle); y within
 1e-2 relative L2 and 1e-4 of its largest element of the oracle's, and within
 fp32 summation order (1e-5 of its largest element) of the workspace form's.
@@ -78,7 +79,11 @@ def compare(wg, wu, wd, xb, alpha):
     assert si.workspace_check(layer.workspace) == 0
 
 
-def test_noalloc_matches_workspace_form_three_calls_in_a_row():
+def test_noalloc_matches_workspace_form_calls_in_a_row():
+    # 13B shape, one token (groups of more than 512 rows), then smaller calls on the same scratch
+    B = synth.planted_layer(5120, 13824, 0.88, config=4, layer=3)
+    compare(u16(B.w_gate), u16(B.w_up), u16(B.w_down), u16(B.x), 1.0)
+    del B
     L = synth.planted_layer(4096, 11008, 0.9, config=2, layer=5)
     x = synth.batch_tokens(L, 2, config=2)
     compare(u16(L.w_gate), u16(L.w_up), u16(L.w_down), u16(x), 1.0)
