@@ -45,6 +45,7 @@ class _Args:
     (_Args(mlp="block"), "k_owned_7b_block_s0.9"),
     (_Args(mlp="relu"), "k_owned_opt6.7b_relu_s0.9"),
     (_Args(shape="13b"), "k_owned_13b_s0.88"),
+    (_Args(mlp="int8", shape="13b"), "k_owned_13b_int8_s0.88"),
     (_Args(batch=4), "k_owned_7b_b4_union_s0.9"),
     (_Args(batch=8), "k_owned_7b_b8_union_s0.9"),
 ])
@@ -70,7 +71,7 @@ def test_committed_counters_match_the_sources():
     instruction-identical builds of) the current kernel sources, so the
     benchmark reports its traffic."""
     for tag in ("k_owned_7b_s0.9", "k_owned_7b_int8_s0.9", "k_owned_7b_block_s0.9", "k_owned_opt6.7b_relu_s0.9",
-                "k_owned_13b_s0.88", "k_owned_7b_b4_union_s0.9", "k_owned_7b_b8_union_s0.9"):
+                "k_owned_13b_s0.88", "k_owned_13b_int8_s0.88", "k_owned_7b_b4_union_s0.9", "k_owned_7b_b8_union_s0.9"):
         assert bench.measured_traffic(os.path.join(ROOT, "profiles", tag + "_counters.txt")) is not None, tag
 
 
