@@ -92,8 +92,11 @@ constexpr int kODN = 8;            // W_down^T pieces per wave and down round
 // 7B-shaped groups of 384 rows 12.33 / 12.23 / 12.18 / 12.41 with batches of
 // 6 / 8 / 10 / 12, INT8 12.23 / 11.87 / 11.76 / 11.94 / 12.54 with 4 / 6 /
 // 8 / 10 / 16; 13B-shaped groups of 560 rows 17.71 / 17.60 / 18.04 with
-// 10 / 12 / 14)
-constexpr int kODN1 = 10;
+// 10 / 12 / 14; with the one-pass fold, on one box: 7B 12.12 / 12.16 /
+// 12.13 / 12.21, decoder-block call 12.67 / 12.75 / 12.74 / 12.80, and the
+// OPT-shaped non-gated call 13.18 / 12.70 / 12.45 / 12.63 with 7 / 8 / 9 /
+// 10, while 11 was 0.05 us slower than 10 at 7B)
+constexpr int kODN1 = 9;
 constexpr int kODN1Int8 = 8;
 constexpr int kODN1Wide = 12;
 static_assert(kODN1 < kWave && kODN1Int8 < kWave && kODN1Wide < kWave, "a wave's last lane polls the tile's zero flag");
